@@ -1,0 +1,216 @@
+"""CPU oracle for the UltraTex foreground hot path -- TEST INFRASTRUCTURE ONLY.
+
+Only the tests, the package smoke check and the benchmark's CPU-baseline leg
+may import this module. The product path (the HIP library and its Python
+binding) never imports, calls or links it, and this module imports nothing of
+the product path: the two share no code. Inputs come from `workloads`, which
+holds none of the method's arithmetic.
+
+Every function is a plain, slow, direct statement of what the paper defines,
+in float64 (bf16 inputs are upcast exactly). Where the paper is silent the
+reading taken is stated in the docstring.
+
+Paper sections (arXiv 2609.23169, "UltraTex"):
+  * Background Token Dropping: Sec. 3.2, "Mask Construction and Sequence
+    Compression" (retained positions M_fg, the Gather_{M_fg} operator that
+    concatenates them) and "Efficient Inference" (Eq. 4: only positions in M_fg
+    are written back; Eq. 9: the composite latent keeps every other position).
+  * Block-Sparse Attention: Sec. 3.3, Eq. 5 (dense softmax attention with
+    scale 1/sqrt(d)), the b_q / b_kv block partition, Eq. 7 (binary block mask
+    M_c) and Eq. 8 (each query block attends only to its selected key blocks).
+  * The backward pass: the paper trains its third stage with block-sparse
+    attention but prints no gradient formula; the oracle differentiates Eq. 8
+    with the mask held constant (the standard softmax-attention gradient
+    restricted to the retained pairs).
+"""
+from __future__ import annotations
+
+import numpy as np
+
+__all__ = [
+    "compact", "gather", "scatter", "block_index",
+    "bsattn_fwd", "bsattn_bwd",
+]
+
+
+# ---------------------------------------------------------------------------
+# Background Token Dropping (Sec. 3.2)
+# ---------------------------------------------------------------------------
+
+def compact(fg_mask) -> tuple[np.ndarray, np.ndarray, int]:
+    """The retained set M_fg of a flat per-view foreground mask.
+
+    Returns (kept_idx, inv_idx, n_kept): kept_idx lists the positions p with a
+    nonzero mask byte in ascending p (the paper concatenates the retained
+    tokens; ascending original order is the reading taken, view-major and
+    row-major as the unified sequence is laid out); inv_idx[p] is the packed
+    index of p, or -1 for a dropped position.
+    """
+    flags = np.asarray(fg_mask).reshape(-1).tolist()
+    inv = np.full(len(flags), -1, dtype=np.int32)
+    kept = []
+    for p, f in enumerate(flags):
+        if f != 0:
+            inv[p] = len(kept)
+            kept.append(p)
+    return np.asarray(kept, dtype=np.int32), inv, len(kept)
+
+
+def gather(x_full: np.ndarray, kept_idx: np.ndarray) -> np.ndarray:
+    """Gather_{M_fg}: packed row k is full row kept_idx[k] (a byte copy)."""
+    return np.asarray(x_full)[np.asarray(kept_idx, dtype=np.int64)]
+
+
+def scatter(x_packed: np.ndarray, kept_idx: np.ndarray,
+            x_full_prefilled: np.ndarray) -> np.ndarray:
+    """Write packed row k back to full row kept_idx[k]; every other row keeps
+    its prior contents (the background noise of Eq. 4, or z_bg of Eq. 9)."""
+    out = np.array(x_full_prefilled, copy=True)
+    out[np.asarray(kept_idx, dtype=np.int64)] = x_packed
+    return out
+
+
+# ---------------------------------------------------------------------------
+# Block index (Sec. 3.3, Eq. 7 and the sets S_i of Eq. 8)
+# ---------------------------------------------------------------------------
+
+def block_index(block_mask: np.ndarray):
+    """Row lists S_i and their transpose from a block mask [B, H, Nq, Nk].
+
+    Returns (rowptr, cols, colptr, rows) as int32 arrays. Row r = (b*H + h)*Nq
+    + i lists S_i = {j : M_c[b,h,i,j] = 1} in ascending j between rowptr[r]
+    and rowptr[r+1]. Column c = (b*H + h)*Nk + j lists {i : M_c[b,h,i,j] = 1}
+    in ascending i between colptr[c] and colptr[c+1].
+    """
+    m = np.asarray(block_mask)
+    B, H, Nq, Nk = m.shape
+    rowptr, cols = [0], []
+    for b in range(B):
+        for h in range(H):
+            for i in range(Nq):
+                s_i = np.flatnonzero(m[b, h, i, :])
+                cols.extend(s_i.tolist())
+                rowptr.append(len(cols))
+    colptr, rows = [0], []
+    for b in range(B):
+        for h in range(H):
+            for j in range(Nk):
+                t_j = np.flatnonzero(m[b, h, :, j])
+                rows.extend(t_j.tolist())
+                colptr.append(len(rows))
+    as32 = lambda a: np.asarray(a, dtype=np.int32)
+    return as32(rowptr), as32(cols), as32(colptr), as32(rows)
+
+
+# ---------------------------------------------------------------------------
+# Block-sparse attention (Sec. 3.3, Eq. 5 and Eq. 8)
+# ---------------------------------------------------------------------------
+
+def _f64(x) -> np.ndarray:
+    """Exact upcast of a bf16 torch tensor (or any array) to float64."""
+    try:
+        import torch
+        if isinstance(x, torch.Tensor):
+            return x.detach().to(torch.float64).numpy()
+    except ImportError:  # pragma: no cover
+        pass
+    return np.asarray(x, dtype=np.float64)
+
+
+def _block_tokens(j: int, block: int, n: int) -> np.ndarray:
+    """Token rows of block j: the partition of Sec. 3.3, with a shorter last
+    block when N is not a multiple of the block size (the paper assumes
+    divisibility; a ragged tail is the reading taken)."""
+    return np.arange(j * block, min(n, (j + 1) * block))
+
+
+def _selected_keys(mask_row: np.ndarray, block: int, n: int) -> np.ndarray:
+    """Token indices of all key blocks in S_i, ascending."""
+    sel = np.flatnonzero(mask_row)
+    if sel.size == 0:
+        return np.zeros(0, dtype=np.int64)
+    return np.concatenate([_block_tokens(j, block, n) for j in sel])
+
+
+def bsattn_fwd(q, k, v, block_mask, block: int, scale: float,
+               q_blocks=None):
+    """Eq. 8: O_i = softmax(Q_i K_{S_i}^T * scale) V_{S_i} per (batch, head,
+    query block i), plus the natural-log log-sum-exp of each query row's
+    scaled scores over the keys it attends to.
+
+    q, k, v: [B, N, H, D]; block_mask: [B, H, Nq, Nk] with Nq = Nk =
+    ceil(N / block). q_blocks: optional iterable of query-block indices to
+    compute (rows of other blocks are left NaN). A query block whose S_i is
+    empty attends to nothing: its rows are O = 0 and LSE = -inf (the paper
+    never produces such a row; this is the reading taken).
+
+    Returns (O [B, N, H, D], LSE [B, H, N]) in float64.
+    """
+    Q, K, V = _f64(q), _f64(k), _f64(v)
+    m = np.asarray(block_mask)
+    B, N, H, D = Q.shape
+    Nq = m.shape[2]
+    O = np.full((B, N, H, D), np.nan)
+    LSE = np.full((B, H, N), np.nan)
+    blocks = range(Nq) if q_blocks is None else q_blocks
+    for b in range(B):
+        for h in range(H):
+            for i in blocks:
+                rows = _block_tokens(i, block, N)
+                keys = _selected_keys(m[b, h, i], block, N)
+                if keys.size == 0:
+                    O[b, rows, h, :] = 0.0
+                    LSE[b, h, rows] = -np.inf
+                    continue
+                S = (Q[b, rows, h, :] @ K[b, keys, h, :].T) * scale
+                mx = S.max(axis=1, keepdims=True)
+                E = np.exp(S - mx)
+                l = E.sum(axis=1, keepdims=True)
+                O[b, rows, h, :] = (E @ V[b, keys, h, :]) / l
+                LSE[b, h, rows] = mx[:, 0] + np.log(l[:, 0])
+    return O, LSE
+
+
+def bsattn_bwd(q, k, v, dout, block_mask, block: int, scale: float,
+               q_blocks=None):
+    """Gradients of Eq. 8 for a loss whose gradient w.r.t. O is dout.
+
+    The block mask is a constant. With P = softmax(S) over the retained keys of
+    each row, S = Q K^T * scale:
+        dV = P^T dO,   dP = dO V^T,   delta_r = sum_c P_rc dP_rc,
+        dS = P o (dP - delta),   dQ = scale * dS K,   dK = scale * dS^T Q.
+    Pairs outside the mask contribute nothing. Rows with an empty S_i have
+    zero gradients.
+
+    q_blocks: optional subset of query blocks whose contributions are summed
+    (dQ of other rows is NaN; dK and dV then hold only the listed blocks'
+    contributions). Returns (dQ, dK, dV) [B, N, H, D] float64.
+    """
+    Q, K, V, dO = _f64(q), _f64(k), _f64(v), _f64(dout)
+    m = np.asarray(block_mask)
+    B, N, H, D = Q.shape
+    Nq = m.shape[2]
+    dQ = np.full((B, N, H, D), np.nan)
+    dK = np.zeros((B, N, H, D))
+    dV = np.zeros((B, N, H, D))
+    blocks = range(Nq) if q_blocks is None else q_blocks
+    for b in range(B):
+        for h in range(H):
+            for i in blocks:
+                rows = _block_tokens(i, block, N)
+                keys = _selected_keys(m[b, h, i], block, N)
+                dQ[b, rows, h, :] = 0.0
+                if keys.size == 0:
+                    continue
+                Qi, Kk, Vk, dOi = Q[b, rows, h], K[b, keys, h], V[b, keys, h], dO[b, rows, h]
+                S = (Qi @ Kk.T) * scale
+                E = np.exp(S - S.max(axis=1, keepdims=True))
+                P = E / E.sum(axis=1, keepdims=True)
+                dP = dOi @ Vk.T
+                delta = (P * dP).sum(axis=1, keepdims=True)
+                dS = P * (dP - delta)
+                dQ[b, rows, h, :] = scale * (dS @ Kk)
+                dK[b, keys, h, :] += scale * (dS.T @ Qi)
+                dV[b, keys, h, :] += P.T @ dOi
+    return dQ, dK, dV
+

@@ -1,0 +1,354 @@
+"""Pins of the CPU oracle against what the paper and the mathematics fix.
+
+None of these re-calls the oracle's own formula or library routine: each pin
+is an independent route (a different library routine, a closed form worked
+out by hand, brute force over scalars, finite differences, or an invariant),
+chosen so that a dropped term, a wrong sign or index, or a transposed operand
+in the oracle fails at least one of them.
+"""
+import math
+
+import numpy as np
+import pytest
+import scipy.sparse as sp
+import torch
+
+import oracle
+import workloads as W
+
+pytestmark = pytest.mark.filterwarnings("ignore::RuntimeWarning")
+
+
+# ---------------------------------------------------------------------------
+# Compaction / gather / scatter (Sec. 3.2)
+# ---------------------------------------------------------------------------
+
+@pytest.mark.parametrize("L,p", [(0, 0.5), (1, 1.0), (1, 0.0), (777, 0.0), (777, 1.0),
+                                 (4097, 0.3), (20000, 0.5), (65537, 0.02)])
+def test_compact_matches_flatnonzero(L, p):
+    rng = np.random.default_rng(L)
+    mask = (rng.random(L) < p).astype(np.uint8) * rng.integers(1, 256, L).astype(np.uint8)
+    kept, inv, n = oracle.compact(mask)
+    ref = np.flatnonzero(mask)
+    assert n == ref.size
+    assert np.array_equal(kept, ref.astype(np.int32))
+    # inverse map: dropped positions are -1, kept positions invert kept_idx
+    assert np.all(inv[mask == 0] == -1)
+    assert np.array_equal(inv[ref], np.arange(n, dtype=np.int32))
+
+
+def test_compact_workload_masks():
+    for name in ("tiny", "c512"):
+        inst = W.make(W.WORKLOADS[name], with_qkv=False)
+        kept, inv, n = oracle.compact(inst.fg_mask)
+        assert n == inst.n_kept == int(inst.fg_mask.astype(bool).sum())
+        assert np.all(np.diff(kept) > 0)
+
+
+def test_gather_scatter_against_boolean_indexing():
+    rng = np.random.default_rng(7)
+    L, C = 3000, 40
+    mask = (rng.random(L) < 0.37).astype(np.uint8)
+    # random 16-bit patterns, NaNs included: compared bitwise
+    x = rng.integers(0, 1 << 16, size=(L, C), dtype=np.uint16)
+    kept, _, n = oracle.compact(mask)
+    packed = oracle.gather(x, kept)
+    assert np.array_equal(packed, x[mask.astype(bool)])
+    prefill = rng.integers(0, 1 << 16, size=(L, C), dtype=np.uint16)
+    out = oracle.scatter(packed, kept, prefill)
+    assert np.array_equal(out[mask.astype(bool)], x[mask.astype(bool)])
+    assert np.array_equal(out[~mask.astype(bool)], prefill[~mask.astype(bool)])
+
+
+# ---------------------------------------------------------------------------
+# Block index (Eq. 7, the sets S_i of Eq. 8)
+# ---------------------------------------------------------------------------
+
+@pytest.mark.parametrize("B,H,Nq,Nk,p", [(1, 1, 1, 1, 1.0), (1, 3, 7, 7, 0.3),
+                                         (2, 2, 13, 9, 0.5), (1, 4, 33, 33, 0.0),
+                                         (1, 2, 50, 50, 1.0)])
+def test_block_index_matches_scipy(B, H, Nq, Nk, p):
+    rng = np.random.default_rng(B * 1000 + Nq)
+    m = (rng.random((B, H, Nq, Nk)) < p).astype(np.uint8)
+    rowptr, cols, colptr, rows = oracle.block_index(m)
+    # row lists: CSR of each (b, h) slab, offsets chained across slabs
+    r_ptr, r_idx, c_ptr, c_idx = [0], [], [0], []
+    for b in range(B):
+        for h in range(H):
+            csr = sp.csr_matrix(m[b, h])
+            csr.sort_indices()
+            r_ptr.extend((csr.indptr[1:] + r_ptr[-1]).tolist())
+            r_idx.extend(csr.indices.tolist())
+            csc = sp.csc_matrix(m[b, h])
+            csc.sort_indices()
+            c_ptr.extend((csc.indptr[1:] + c_ptr[-1]).tolist())
+            c_idx.extend(csc.indices.tolist())
+    assert np.array_equal(rowptr, np.array(r_ptr, dtype=np.int32))
+    assert np.array_equal(cols, np.array(r_idx, dtype=np.int32))
+    assert np.array_equal(colptr, np.array(c_ptr, dtype=np.int32))
+    assert np.array_equal(rows, np.array(c_idx, dtype=np.int32))
+    assert rowptr[-1] == colptr[-1] == int(m.astype(bool).sum())
+
+
+def test_block_index_brute_force_tiny():
+    m = np.array([[[[1, 0, 1], [0, 0, 0], [1, 1, 1]]]], dtype=np.uint8)
+    rowptr, cols, colptr, rows = oracle.block_index(m)
+    assert rowptr.tolist() == [0, 2, 2, 5]
+    assert cols.tolist() == [0, 2, 0, 1, 2]
+    assert colptr.tolist() == [0, 2, 3, 5]
+    assert rows.tolist() == [0, 2, 2, 0, 2]
+
+
+def test_synthetic_block_mask_row_counts():
+    # Eq. 7 keeps floor(rho * N_k) key blocks per row; the synthetic stand-in
+    # keeps the diagonal plus that many others.
+    rng = np.random.default_rng(0)
+    for rho, nk, koff in (("0.1", 624, 62), ("0.3", 50, 15), ("0.4", 6, 2), ("0.2", 177, 35),
+                          ("0.05", 603, 30)):
+        assert W.kept_off_diagonal(rho, nk) == koff
+        bm = W.block_mask(1, 3, nk, nk, rho, rng)
+        assert np.all(bm.sum(-1) == koff + 1)
+        assert np.all(bm[0, :, np.arange(nk), np.arange(nk)] == 1)
+
+
+# ---------------------------------------------------------------------------
+# Forward (Eq. 5, Eq. 8)
+# ---------------------------------------------------------------------------
+
+def _expand_mask(bm, n, block):
+    """Token-level boolean mask [B, H, N, N] from a block mask."""
+    tok = np.arange(n) // block
+    return bm[:, :, tok][:, :, :, tok].astype(bool)
+
+
+def _sdpa(q, k, v, tokmask=None):
+    """torch's scaled_dot_product_attention in float64 on [B, N, H, D] inputs."""
+    t = lambda a: torch.as_tensor(a, dtype=torch.float64).permute(0, 2, 1, 3)
+    am = None if tokmask is None else torch.as_tensor(tokmask)
+    o = torch.nn.functional.scaled_dot_product_attention(t(q), t(k), t(v), attn_mask=am)
+    return o.permute(0, 2, 1, 3).numpy()
+
+
+def test_fwd_hand_worked_example():
+    """Three tokens, d = 2, block 2 (a short last block). Scores, softmax and
+    outputs below are worked out by hand from Eq. 5 and Eq. 8."""
+    s2 = math.sqrt(2.0)
+    q = np.array([[s2 * math.log(3.0), 0.0], [0.0, 0.0], [0.0, 0.0]])
+    k = np.array([[1.0, 0.0], [0.0, 1.0], [10.0, 10.0]])
+    v = np.array([[1.0, 2.0], [5.0, -2.0], [100.0, 100.0]])
+    bm = np.array([[[[1, 0], [1, 1]]]], dtype=np.uint8)
+    O, L = oracle.bsattn_fwd(q[None, :, None], k[None, :, None], v[None, :, None], bm, 2,
+                             1.0 / s2)
+    # row 0: scores (ln 3, 0) -> P = (3/4, 1/4); key 2 lies in a skipped block
+    assert np.allclose(O[0, 0, 0], [2.0, 1.0], atol=1e-14)
+    assert math.isclose(L[0, 0, 0], math.log(4.0), abs_tol=1e-14)
+    # row 1: zero query -> uniform over keys 0, 1
+    assert np.allclose(O[0, 1, 0], [3.0, 0.0], atol=1e-14)
+    assert math.isclose(L[0, 0, 1], math.log(2.0), abs_tol=1e-14)
+    # row 2: zero query, both blocks selected -> uniform over keys 0, 1, 2
+    assert np.allclose(O[0, 2, 0], [106.0 / 3.0, 100.0 / 3.0], atol=1e-12)
+    assert math.isclose(L[0, 0, 2], math.log(3.0), abs_tol=1e-14)
+
+
+def test_bwd_hand_worked_example():
+    """Same three tokens, dO = e_0 on row 0 only. Hand derivation:
+    dP = (v_0[0], v_1[0]) = (1, 5); delta = 3/4 + 5/4 = 2;
+    dS = P o (dP - delta) = (-3/4, 3/4); dQ_0 = (1/sqrt2) * (-3/4 k_0 + 3/4 k_1);
+    dK_c = (1/sqrt2) dS_c q_0; dV_c = P_c dO_0."""
+    s2 = math.sqrt(2.0)
+    q = np.array([[s2 * math.log(3.0), 0.0], [0.0, 0.0], [0.0, 0.0]])
+    k = np.array([[1.0, 0.0], [0.0, 1.0], [10.0, 10.0]])
+    v = np.array([[1.0, 2.0], [5.0, -2.0], [100.0, 100.0]])
+    do = np.array([[1.0, 0.0], [0.0, 0.0], [0.0, 0.0]])
+    bm = np.array([[[[1, 0], [1, 1]]]], dtype=np.uint8)
+    ex = lambda a: a[None, :, None]
+    dQ, dK, dV = oracle.bsattn_bwd(ex(q), ex(k), ex(v), ex(do), bm, 2, 1.0 / s2)
+    c = 3.0 / (4.0 * s2)
+    assert np.allclose(dQ[0, :, 0], [[-c, c], [0, 0], [0, 0]], atol=1e-14)
+    l3 = math.log(3.0)
+    assert np.allclose(dK[0, :, 0], [[-0.75 * l3, 0], [0.75 * l3, 0], [0, 0]], atol=1e-14)
+    assert np.allclose(dV[0, :, 0], [[0.75, 0], [0.25, 0], [0, 0]], atol=1e-14)
+
+
+@pytest.mark.parametrize("n,block,H,D", [(64, 16, 2, 8), (70, 16, 1, 16), (130, 64, 2, 32)])
+def test_fwd_all_ones_is_dense_sdpa(n, block, H, D):
+    rng = np.random.default_rng(n)
+    q, k, v = (rng.standard_normal((1, n, H, D)) for _ in range(3))
+    nb = -(-n // block)
+    O, L = oracle.bsattn_fwd(q, k, v, np.ones((1, H, nb, nb), np.uint8), block,
+                             1.0 / math.sqrt(D))
+    assert np.allclose(O, _sdpa(q, k, v), atol=1e-12, rtol=1e-12)
+    s = torch.einsum("bnhd,bmhd->bhnm", torch.tensor(q), torch.tensor(k)) / math.sqrt(D)
+    assert np.allclose(L, torch.logsumexp(s, dim=-1).numpy(), atol=1e-12)
+
+
+@pytest.mark.parametrize("seed,n,block,H,D,density", [(1, 70, 16, 2, 16, 0.4),
+                                                      (2, 200, 32, 3, 8, 0.25),
+                                                      (3, 97, 8, 1, 4, 0.6)])
+def test_fwd_masked_matches_sdpa_boolean_mask(seed, n, block, H, D, density):
+    rng = np.random.default_rng(seed)
+    q, k, v = (rng.standard_normal((1, n, H, D)) * 2.0 for _ in range(3))
+    nb = -(-n // block)
+    bm = (rng.random((1, H, nb, nb)) < density).astype(np.uint8)
+    bm[:, :, np.arange(nb), np.arange(nb)] = 1
+    O, _ = oracle.bsattn_fwd(q, k, v, bm, block, 1.0 / math.sqrt(D))
+    ref = _sdpa(q, k, v, _expand_mask(bm, n, block))
+    assert np.allclose(O, ref, atol=1e-12, rtol=1e-12)
+
+
+def test_fwd_diagonal_only_is_blockwise_dense():
+    rng = np.random.default_rng(11)
+    n, block, H, D = 90, 32, 2, 8
+    q, k, v = (rng.standard_normal((1, n, H, D)) for _ in range(3))
+    nb = -(-n // block)
+    bm = np.zeros((1, H, nb, nb), np.uint8)
+    bm[:, :, np.arange(nb), np.arange(nb)] = 1
+    O, _ = oracle.bsattn_fwd(q, k, v, bm, block, 1.0 / math.sqrt(D))
+    for i in range(nb):
+        sl = slice(i * block, min(n, (i + 1) * block))
+        assert np.allclose(O[:, sl], _sdpa(q[:, sl], k[:, sl], v[:, sl]), atol=1e-12)
+
+
+def test_fwd_brute_force_scalar_loops_with_empty_row():
+    """Pure-Python scalar loops over every (row, key) pair, ragged tail and an
+    empty block row included."""
+    rng = np.random.default_rng(5)
+    n, block, D = 23, 5, 3
+    q, k, v = (rng.standard_normal((1, n, 1, D)) for _ in range(3))
+    nb = -(-n // block)
+    bm = (rng.random((1, 1, nb, nb)) < 0.5).astype(np.uint8)
+    bm[0, 0, 2, :] = 0                     # query block 2 attends to nothing
+    bm[0, 0, 0, nb - 1] = 1                # a short key block is selected
+    scale = 0.7
+    O, L = oracle.bsattn_fwd(q, k, v, bm, block, scale)
+    for r in range(n):
+        allowed = [c for c in range(n) if bm[0, 0, r // block, c // block]]
+        if not allowed:
+            assert np.all(O[0, r, 0] == 0) and L[0, 0, r] == -np.inf
+            continue
+        s = {c: scale * sum(q[0, r, 0, d] * k[0, c, 0, d] for d in range(D)) for c in allowed}
+        mx = max(s.values())
+        z = sum(math.exp(s[c] - mx) for c in allowed)
+        for d in range(D):
+            o = sum(math.exp(s[c] - mx) * v[0, c, 0, d] for c in allowed) / z
+            assert math.isclose(O[0, r, 0, d], o, rel_tol=1e-12, abs_tol=1e-12)
+        assert math.isclose(L[0, 0, r], mx + math.log(z), rel_tol=1e-13)
+
+
+def test_fwd_zero_query_is_mean_of_allowed_values():
+    rng = np.random.default_rng(9)
+    n, block, H, D = 77, 16, 2, 8
+    q = np.zeros((1, n, H, D))
+    k, v = (rng.standard_normal((1, n, H, D)) for _ in range(2))
+    nb = -(-n // block)
+    bm = (rng.random((1, H, nb, nb)) < 0.5).astype(np.uint8)
+    bm[:, :, np.arange(nb), np.arange(nb)] = 1
+    O, L = oracle.bsattn_fwd(q, k, v, bm, block, 0.3)
+    for h in range(H):
+        for r in range(n):
+            cols = [c for c in range(n) if bm[0, h, r // block, c // block]]
+            assert np.allclose(O[0, r, h], v[0, cols, h].mean(axis=0), atol=1e-13)
+            assert math.isclose(L[0, h, r], math.log(len(cols)), rel_tol=1e-13)
+
+
+def test_fwd_invariants_unit_values_and_peaky_scores():
+    rng = np.random.default_rng(3)
+    n, block, H, D = 150, 32, 2, 16
+    q = rng.standard_normal((1, n, H, D)) * 40.0    # large scores: online-max stress
+    k = rng.standard_normal((1, n, H, D))
+    nb = -(-n // block)
+    bm = (rng.random((1, H, nb, nb)) < 0.4).astype(np.uint8)
+    bm[:, :, np.arange(nb), np.arange(nb)] = 1
+    O, L = oracle.bsattn_fwd(q, k, np.ones((1, n, H, D)), bm, block, 0.25)
+    assert np.allclose(O, 1.0, atol=1e-12)        # rows of P sum to one
+    assert np.all(np.isfinite(L))
+    v = rng.standard_normal((1, n, H, D))
+    O2, _ = oracle.bsattn_fwd(q, k, v, bm, block, 0.25)
+    tq = torch.tensor(q * 0.25 / (1 / math.sqrt(D)))   # SDPA applies 1/sqrt(D)
+    ref = _sdpa(tq.numpy(), k, v, _expand_mask(bm, n, block))
+    assert np.allclose(O2, ref, atol=1e-10)
+
+
+def test_dropped_tokens_never_influence_kept_outputs():
+    """Background rows of the full sequence set to NaN: after dropping, every
+    kept output is finite and identical to the run with other background."""
+    inst = W.make(W.WORKLOADS["tiny"], with_qkv=False)
+    L, H, D = inst.wl.seq_len, 2, 16
+    rng = np.random.default_rng(1)
+    full = rng.standard_normal((L, 3, H, D))
+    kept, _, n = oracle.compact(inst.fg_mask)
+    a = full.copy()
+    a[inst.fg_mask == 0] = np.nan
+    b = full.copy()
+    b[inst.fg_mask == 0] = 1e6
+    nb = -(-n // 64)
+    bm = np.ones((1, H, nb, nb), np.uint8)
+    outs = []
+    for x in (a, b):
+        p = oracle.gather(x, kept)
+        O, _ = oracle.bsattn_fwd(p[None, :, 0], p[None, :, 1], p[None, :, 2], bm, 64, 0.25)
+        outs.append(O)
+    assert np.all(np.isfinite(outs[0]))
+    assert np.array_equal(outs[0], outs[1])
+
+
+# ---------------------------------------------------------------------------
+# Backward (gradient of Eq. 8, mask constant)
+# ---------------------------------------------------------------------------
+
+@pytest.mark.parametrize("seed,n,block,H,D,density", [(1, 70, 16, 2, 8, 0.4),
+                                                      (4, 129, 32, 1, 16, 0.3)])
+def test_bwd_matches_torch_autograd(seed, n, block, H, D, density):
+    rng = np.random.default_rng(seed)
+    q, k, v, do = (rng.standard_normal((1, n, H, D)) for _ in range(4))
+    nb = -(-n // block)
+    bm = (rng.random((1, H, nb, nb)) < density).astype(np.uint8)
+    bm[:, :, np.arange(nb), np.arange(nb)] = 1
+    tq, tk, tv = (torch.tensor(a, requires_grad=True) for a in (q, k, v))
+    t = lambda a: a.permute(0, 2, 1, 3)
+    o = torch.nn.functional.scaled_dot_product_attention(
+        t(tq), t(tk), t(tv), attn_mask=torch.as_tensor(_expand_mask(bm, n, block)))
+    o.permute(0, 2, 1, 3).backward(torch.tensor(do))
+    dQ, dK, dV = oracle.bsattn_bwd(q, k, v, do, bm, block, 1.0 / math.sqrt(D))
+    assert np.allclose(dQ, tq.grad.numpy(), atol=1e-12)
+    assert np.allclose(dK, tk.grad.numpy(), atol=1e-12)
+    assert np.allclose(dV, tv.grad.numpy(), atol=1e-12)
+
+
+def test_bwd_central_finite_differences():
+    rng = np.random.default_rng(21)
+    n, block, H, D = 19, 6, 1, 3
+    q, k, v, do = (rng.standard_normal((1, n, H, D)) for _ in range(4))
+    nb = -(-n // block)
+    bm = (rng.random((1, H, nb, nb)) < 0.5).astype(np.uint8)
+    bm[0, 0, 1, :] = 0                          # empty row: zero gradients
+    bm[0, 0, 0, 0] = bm[0, 0, 3, 3] = 1
+    scale = 0.8
+
+    def loss(qq, kk, vv):
+        O, _ = oracle.bsattn_fwd(qq, kk, vv, bm, block, scale)
+        return float((O * do).sum())
+
+    dQ, dK, dV = oracle.bsattn_bwd(q, k, v, do, bm, block, scale)
+    h = 1e-5
+    for grad, which in ((dQ, 0), (dK, 1), (dV, 2)):
+        for idx in np.ndindex(q.shape):
+            args = [q.copy(), k.copy(), v.copy()]
+            args[which][idx] += h
+            up = loss(*args)
+            args[which][idx] -= 2 * h
+            dn = loss(*args)
+            assert abs((up - dn) / (2 * h) - grad[idx]) < 1e-7, (which, idx)
+    assert np.all(dQ[0, block:2 * block] == 0)
+
+
+def test_bwd_invariants_sum_dk_zero_sum_dv_equals_sum_do():
+    rng = np.random.default_rng(8)
+    n, block, H, D = 200, 32, 3, 8
+    q, k, v, do = (rng.standard_normal((1, n, H, D)) for _ in range(4))
+    nb = -(-n // block)
+    bm = (rng.random((1, H, nb, nb)) < 0.3).astype(np.uint8)
+    bm[:, :, np.arange(nb), np.arange(nb)] = 1
+    dQ, dK, dV = oracle.bsattn_bwd(q, k, v, do, bm, block, 0.35)
+    assert np.allclose(dK.sum(axis=1), 0.0, atol=1e-11)
+    assert np.allclose(dV.sum(axis=1), do.sum(axis=1), atol=1e-11)
