@@ -1,0 +1,190 @@
+/*
+ * ultratex.h -- C ABI of libultratex.so: the foreground hot path of UltraTex
+ * (arXiv 2609.23169) on one AMD Instinct MI355X (gfx950).
+ *
+ * The path: Background Token Dropping packs the foreground tokens of the
+ * unified multi-view sequence (Sec. 3.2), block lists are built from a block
+ * mask (Sec. 3.3, Eq. 7), block-sparse attention runs forward and backward
+ * over the packed sequence (Sec. 3.3, Eq. 8), and the packed tokens are
+ * written back to the full token grid (Sec. 3.2, Eq. 4; Sec. 3.4, Eq. 9).
+ *
+ * Conventions shared by every call:
+ *  - Pointers are DEVICE pointers unless the name ends in _host.
+ *  - The caller allocates and owns every buffer; the library allocates no
+ *    device memory and keeps no pointer after a call returns. Buffers must
+ *    stay alive until the work queued on `stream` has completed.
+ *  - Every call is asynchronous on `stream` (a hipStream_t; NULL is the null
+ *    stream). The only host synchronisations are the optional *_host outputs,
+ *    which wait for the stream before returning.
+ *  - Arguments are validated before anything is launched. On a bad argument a
+ *    call returns a non-zero ut_status, launches nothing and records a message
+ *    readable with ut_last_error() (per calling thread). A HIP runtime error
+ *    returns UT_ERR_HIP with the HIP error text. No C++ exception crosses the
+ *    ABI.
+ *  - Token and block indices are int32; byte offsets are computed in 64 bits.
+ *  - bf16 is IEEE binary32 truncated to its upper 16 bits (stored as uint16),
+ *    results rounded to nearest even.
+ */
+#ifndef ULTRATEX_H
+#define ULTRATEX_H
+
+#include <stddef.h>
+#include <stdint.h>
+#include <hip/hip_runtime_api.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define UT_ABI_VERSION 1
+
+typedef enum {
+  UT_OK = 0,
+  UT_ERR_INVALID_ARG = 1, /* null / misaligned pointer, bad size or count   */
+  UT_ERR_UNSUPPORTED = 2, /* a head_dim or block size the kernels lack      */
+  UT_ERR_WORKSPACE = 3,   /* workspace missing or smaller than required     */
+  UT_ERR_CAPACITY = 4,    /* an output holds fewer entries than produced    */
+  UT_ERR_HIP = 5          /* a HIP runtime or launch error                  */
+} ut_status;
+
+/* Message for the last non-OK status returned on this thread ("" if none). */
+const char* ut_last_error(void);
+
+/* UT_ABI_VERSION of the loaded library. */
+int ut_abi_version(void);
+
+/* ------------------------------------------------------------------------
+ * Background Token Dropping (Sec. 3.2, "Mask Construction and Sequence
+ * Compression"): the retained set M_fg of a per-view token-grid foreground
+ * mask and the Gather_{M_fg} of a full-sequence hidden state.
+ *
+ * fg_mask     [L] uint8, the unified sequence's token-grid masks laid out
+ *             view-major then row-major; nonzero = foreground (kept).
+ * x_full      [L, row_bytes] rows to gather, or NULL for the index map only.
+ * row_bytes   bytes per row; a positive multiple of 16 (e.g. 3072 bf16 =
+ *             6144). x_full and x_packed must be 16-byte aligned.
+ * x_packed    [capacity, row_bytes] output; NULL iff x_full is NULL.
+ * capacity    rows available in kept_idx and x_packed.
+ * kept_idx    [capacity] int32 output: kept positions in ascending order
+ *             (packed row k is full row kept_idx[k]).
+ * inv_idx     [L] int32 output (NULL to skip): packed index of each position,
+ *             -1 where dropped.
+ * n_kept      [1] int32 device output: the number of kept positions (written
+ *             even when it exceeds capacity; then only `capacity` entries are
+ *             written and the host cannot tell without reading it).
+ * n_kept_host optional host output: if non-NULL the call waits for the stream,
+ *             stores the count, and returns UT_ERR_CAPACITY if it exceeds
+ *             capacity.
+ * workspace   device scratch of ut_drop_background_workspace_size(L) bytes,
+ *             4-byte aligned; contents need not be initialised.
+ * Errors: L < 1 or L >= 2^31, null required pointers, row_bytes not a
+ *         positive multiple of 16, misalignment, capacity < 0 ->
+ *         UT_ERR_INVALID_ARG; workspace too small -> UT_ERR_WORKSPACE.
+ * ---------------------------------------------------------------------- */
+size_t ut_drop_background_workspace_size(int64_t L);
+ut_status ut_drop_background(const uint8_t* fg_mask, int64_t L,
+                             const void* x_full, int64_t row_bytes,
+                             void* x_packed, int64_t capacity,
+                             int32_t* kept_idx, int32_t* inv_idx,
+                             int32_t* n_kept, int64_t* n_kept_host,
+                             void* workspace, size_t workspace_bytes,
+                             hipStream_t stream);
+
+/* ------------------------------------------------------------------------
+ * Write-back of the packed foreground rows (Sec. 3.2, Eq. 4: only positions
+ * in M_fg are updated; Sec. 3.4, Eq. 9: every other position keeps the
+ * background the caller pre-filled, Gaussian noise or the tiled z_bg).
+ *
+ * x_packed  [n_kept, row_bytes] rows to write.
+ * kept_idx  [n_kept] int32 full-sequence positions, each in [0, L); the
+ *           positions must be distinct (as ut_drop_background produces).
+ * row_bytes positive multiple of 16; both row buffers 16-byte aligned.
+ * x_full    [L, row_bytes] in/out: row kept_idx[k] <- packed row k; rows not
+ *           listed are untouched.
+ * n_kept = 0 is a no-op. kept_idx contents are trusted (not range-checked).
+ * ---------------------------------------------------------------------- */
+ut_status ut_scatter_foreground(const void* x_packed, const int32_t* kept_idx,
+                                int64_t n_kept, int64_t row_bytes, void* x_full,
+                                hipStream_t stream);
+
+/* ------------------------------------------------------------------------
+ * Block index (Sec. 3.3, Eq. 7; the sets S_i of Eq. 8): from a binary block
+ * mask M_c per (batch, head), the list of selected key blocks of every query
+ * block (ascending j) and the transpose, the list of query blocks that select
+ * each key block (ascending i), both in compressed-row form.
+ *
+ * block_mask [B, H, Nq, Nk] uint8, nonzero = the pair (i, j) is computed.
+ * q_rowptr   [B*H*Nq + 1] int32 out: row r = (b*H + h)*Nq + i spans
+ *            q_cols[q_rowptr[r] .. q_rowptr[r+1]).
+ * q_cols     [cap] int32 out: key-block indices j.
+ * kv_colptr  [B*H*Nk + 1] int32 out: column c = (b*H + h)*Nk + j spans
+ *            kv_rows[kv_colptr[c] .. kv_colptr[c+1]).
+ * kv_rows    [cap] int32 out: query-block indices i.
+ * cap        entries available in q_cols and kv_rows; entries past cap are
+ *            not written.
+ * nnz_host   optional: if non-NULL the call waits, stores the number of
+ *            nonzero mask entries, and returns UT_ERR_CAPACITY if > cap.
+ * Errors: any of B, H, Nq, Nk < 1, B*H*max(Nq,Nk) >= 2^31, null pointers ->
+ *         UT_ERR_INVALID_ARG.
+ * ---------------------------------------------------------------------- */
+ut_status ut_build_block_index(const uint8_t* block_mask, int32_t B, int32_t H,
+                               int32_t Nq, int32_t Nk, int32_t* q_rowptr,
+                               int32_t* q_cols, int32_t* kv_colptr,
+                               int32_t* kv_rows, int64_t cap, int64_t* nnz_host,
+                               hipStream_t stream);
+
+/* ------------------------------------------------------------------------
+ * Block-sparse attention forward (Sec. 3.3, Eq. 5 and Eq. 8): for each
+ * (batch b, head h, query block i), O_i = softmax(Q_i K_{S_i}^T * scale)
+ * V_{S_i}; key blocks outside S_i are never read.
+ *
+ * q, k, v   bf16 [B, N, H, D] contiguous (token-major, heads interleaved:
+ *           the layout of a [N, H*D] projection output), 16-byte aligned.
+ * o         bf16 [B, N, H, D] output.
+ * lse       fp32 [B, H, N] output: natural-log log-sum-exp of each query
+ *           row's scaled scores over its retained keys; -inf for a row whose
+ *           S_i is empty (its O row is 0).
+ * D         head_dim, 64 or 128. block: b_q = b_kv, 64 or 128.
+ * Nq = Nk = ceil(N / block); the last block may be short (keys beyond N are
+ *           excluded, rows beyond N are neither computed nor stored).
+ * q_rowptr, q_cols  the row lists of ut_build_block_index for [B, H, Nq, Nq].
+ *           Contents are trusted: each j must lie in [0, Nq).
+ * softmax_scale  the score scale, 1/sqrt(D) in the paper.
+ * Errors: unsupported D / block -> UT_ERR_UNSUPPORTED; N < 1, B or H < 1,
+ *         null or misaligned pointers, non-finite scale -> UT_ERR_INVALID_ARG.
+ * ---------------------------------------------------------------------- */
+ut_status ut_bsattn_fwd(const void* q, const void* k, const void* v, void* o,
+                        float* lse, int32_t B, int32_t N, int32_t H, int32_t D,
+                        int32_t block, const int32_t* q_rowptr,
+                        const int32_t* q_cols, float softmax_scale,
+                        hipStream_t stream);
+
+/* ------------------------------------------------------------------------
+ * Block-sparse attention backward: gradients of Eq. 8 with the block mask
+ * held constant (the paper's third training stage runs this attention; it
+ * prints no gradient formula). With P = softmax of the retained scores:
+ * dV = P^T dO, dP = dO V^T, delta = rowsum(dO o O), dS = P o (dP - delta),
+ * dQ = scale dS K, dK = scale dS^T Q. No atomics: results are deterministic.
+ *
+ * q, k, v, o, dout  bf16 [B, N, H, D] (o and lse from ut_bsattn_fwd).
+ * lse               fp32 [B, H, N].
+ * dq, dk, dv        bf16 [B, N, H, D] outputs (fully overwritten).
+ * q_rowptr, q_cols, kv_colptr, kv_rows  both lists of ut_build_block_index.
+ * workspace         device scratch of ut_bsattn_bwd_workspace_size(B, N, H)
+ *                   bytes, 16-byte aligned (holds delta).
+ * Errors: as ut_bsattn_fwd, plus UT_ERR_WORKSPACE.
+ * ---------------------------------------------------------------------- */
+size_t ut_bsattn_bwd_workspace_size(int32_t B, int32_t N, int32_t H);
+ut_status ut_bsattn_bwd(const void* q, const void* k, const void* v,
+                        const void* o, const void* dout, const float* lse,
+                        void* dq, void* dk, void* dv, int32_t B, int32_t N,
+                        int32_t H, int32_t D, int32_t block,
+                        const int32_t* q_rowptr, const int32_t* q_cols,
+                        const int32_t* kv_colptr, const int32_t* kv_rows,
+                        float softmax_scale, void* workspace,
+                        size_t workspace_bytes, hipStream_t stream);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* ULTRATEX_H */

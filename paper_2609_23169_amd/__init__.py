@@ -1,0 +1,281 @@
+"""Python binding of libultratex.so: UltraTex's foreground hot path on MI355X.
+
+The functions `ut_*` mirror the C ABI in include/ultratex.h one to one: they
+take torch tensors, check device, dtype and sizes (a raw pointer cannot carry
+its size), pass the pointers and the current HIP stream, and return the
+ut_status code. Every step of the path runs in the HIP kernels of the
+library; there is no CPU fallback, and importing the package without the
+built library raises.
+
+The helpers below the raw calls (`drop_background`, `build_block_index`,
+`bsattn_fwd`, ...) allocate the outputs and workspaces with torch and raise
+UltraTexError on a non-zero status.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+
+import torch
+
+HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(HERE, "libultratex.so")
+
+UT_OK, UT_ERR_INVALID_ARG, UT_ERR_UNSUPPORTED, UT_ERR_WORKSPACE, UT_ERR_CAPACITY, UT_ERR_HIP = range(6)
+STATUS_NAMES = ["UT_OK", "UT_ERR_INVALID_ARG", "UT_ERR_UNSUPPORTED", "UT_ERR_WORKSPACE",
+                "UT_ERR_CAPACITY", "UT_ERR_HIP"]
+
+# Every symbol the header declares (checked by the CPU test suite).
+EXPORTS = [
+    "ut_last_error", "ut_abi_version",
+    "ut_drop_background_workspace_size", "ut_drop_background",
+    "ut_scatter_foreground", "ut_build_block_index",
+    "ut_bsattn_fwd", "ut_bsattn_bwd_workspace_size", "ut_bsattn_bwd",
+]
+
+
+class UltraTexError(RuntimeError):
+    def __init__(self, fn: str, status: int, msg: str):
+        super().__init__(f"{fn} -> {STATUS_NAMES[status] if 0 <= status < 6 else status}: {msg}")
+        self.status = status
+
+
+_c = ctypes
+_vp, _i32, _i64, _f32, _sz = _c.c_void_p, _c.c_int32, _c.c_int64, _c.c_float, _c.c_size_t
+_SIGS = {
+    "ut_last_error": (_c.c_char_p, []),
+    "ut_abi_version": (_c.c_int, []),
+    "ut_drop_background_workspace_size": (_sz, [_i64]),
+    "ut_drop_background": (_c.c_int, [_vp, _i64, _vp, _i64, _vp, _i64, _vp, _vp, _vp, _vp, _vp, _sz, _vp]),
+    "ut_scatter_foreground": (_c.c_int, [_vp, _vp, _i64, _i64, _vp, _vp]),
+    "ut_build_block_index": (_c.c_int, [_vp, _i32, _i32, _i32, _i32, _vp, _vp, _vp, _vp, _i64, _vp, _vp]),
+    "ut_bsattn_fwd": (_c.c_int, [_vp, _vp, _vp, _vp, _vp, _i32, _i32, _i32, _i32, _i32, _vp, _vp, _f32, _vp]),
+    "ut_bsattn_bwd_workspace_size": (_sz, [_i32, _i32, _i32]),
+    "ut_bsattn_bwd": (_c.c_int, [_vp, _vp, _vp, _vp, _vp, _vp, _vp, _vp, _vp, _i32, _i32, _i32, _i32, _i32,
+                                 _vp, _vp, _vp, _vp, _f32, _vp, _sz, _vp]),
+}
+
+_lib = None
+
+
+def lib() -> ctypes.CDLL:
+    """The loaded library; raises if it has not been built."""
+    global _lib
+    if _lib is None:
+        if not os.path.exists(LIB_PATH):
+            raise RuntimeError(f"{LIB_PATH} is missing: build it with `python -c "
+                               f"'import __graft_entry__ as g; g.build()'`")
+        l = ctypes.CDLL(LIB_PATH)
+        for name, (res, args) in _SIGS.items():
+            f = getattr(l, name)
+            f.restype, f.argtypes = res, args
+        _lib = l
+    return _lib
+
+
+def last_error() -> str:
+    return lib().ut_last_error().decode()
+
+
+def _p(t):
+    """Pointer of a device tensor (None -> NULL)."""
+    if t is None:
+        return None
+    if not isinstance(t, torch.Tensor):
+        raise TypeError("expected a torch.Tensor")
+    if not t.is_cuda:
+        raise ValueError("tensor must live in GPU memory")
+    if not t.is_contiguous():
+        raise ValueError("tensor must be contiguous")
+    return t.data_ptr()
+
+
+def _stream(stream):
+    s = stream if stream is not None else torch.cuda.current_stream()
+    return ctypes.c_void_p(s.cuda_stream)
+
+
+def _need(cond: bool, msg: str):
+    if not cond:
+        raise ValueError(msg)
+
+
+def _nbytes(t) -> int:
+    return t.numel() * t.element_size()
+
+
+# ---------------------------------------------------------------------------
+# Raw calls: same names and argument order as the C ABI, tensors for pointers.
+# ---------------------------------------------------------------------------
+
+def ut_drop_background_workspace_size(L: int) -> int:
+    return int(lib().ut_drop_background_workspace_size(L))
+
+
+def ut_drop_background(fg_mask, x_full, x_packed, kept_idx, inv_idx, n_kept, workspace,
+                       n_kept_host: bool = False, stream=None):
+    """Returns (status, n_kept or None)."""
+    L = fg_mask.numel()
+    _need(fg_mask.dtype == torch.uint8, "fg_mask must be uint8")
+    capacity = kept_idx.numel()
+    _need(kept_idx.dtype == torch.int32 and n_kept.dtype == torch.int32 and n_kept.numel() >= 1,
+          "kept_idx and n_kept must be int32")
+    row_bytes = 0
+    if x_full is not None:
+        _need(x_packed is not None, "x_packed needed with x_full")
+        _need(x_full.dim() >= 1 and x_full.shape[0] == L, "x_full must have L rows")
+        row_bytes = _nbytes(x_full) // L
+        _need(x_packed.shape[0] >= capacity and _nbytes(x_packed) >= capacity * row_bytes
+              and x_packed.dtype == x_full.dtype, "x_packed must hold capacity rows")
+    if inv_idx is not None:
+        _need(inv_idx.dtype == torch.int32 and inv_idx.numel() >= L, "inv_idx must be int32 [L]")
+    host = ctypes.c_int64(-1)
+    ws_bytes = _nbytes(workspace) if workspace is not None else 0
+    st = lib().ut_drop_background(_p(fg_mask), L, _p(x_full), row_bytes, _p(x_packed), capacity,
+                                  _p(kept_idx), _p(inv_idx), _p(n_kept),
+                                  ctypes.byref(host) if n_kept_host else None,
+                                  _p(workspace), ws_bytes, _stream(stream))
+    return st, (host.value if n_kept_host else None)
+
+
+def ut_scatter_foreground(x_packed, kept_idx, n_kept: int, x_full, stream=None) -> int:
+    L = x_full.shape[0]
+    row_bytes = _nbytes(x_full) // max(L, 1)
+    _need(kept_idx.dtype == torch.int32 and kept_idx.numel() >= n_kept, "kept_idx int32 [n_kept]")
+    _need(x_packed.dtype == x_full.dtype and _nbytes(x_packed) >= n_kept * row_bytes,
+          "x_packed must hold n_kept rows of x_full's width")
+    return lib().ut_scatter_foreground(_p(x_packed), _p(kept_idx), n_kept, row_bytes, _p(x_full),
+                                       _stream(stream))
+
+
+def ut_build_block_index(block_mask, q_rowptr, q_cols, kv_colptr, kv_rows, nnz_host: bool = False,
+                         stream=None):
+    """Returns (status, nnz or None)."""
+    _need(block_mask.dtype == torch.uint8 and block_mask.dim() == 4, "block_mask uint8 [B,H,Nq,Nk]")
+    B, H, Nq, Nk = block_mask.shape
+    _need(q_rowptr.numel() >= B * H * Nq + 1 and kv_colptr.numel() >= B * H * Nk + 1,
+          "row/column pointer arrays too short")
+    cap = min(q_cols.numel(), kv_rows.numel())
+    for t in (q_rowptr, q_cols, kv_colptr, kv_rows):
+        _need(t.dtype == torch.int32, "index arrays must be int32")
+    host = ctypes.c_int64(-1)
+    st = lib().ut_build_block_index(_p(block_mask), B, H, Nq, Nk, _p(q_rowptr), _p(q_cols),
+                                    _p(kv_colptr), _p(kv_rows), cap,
+                                    ctypes.byref(host) if nnz_host else None, _stream(stream))
+    return st, (host.value if nnz_host else None)
+
+
+def _attn_shape(q, block):
+    _need(q.dim() == 4, "q/k/v must be [B, N, H, D]")
+    B, N, H, D = q.shape
+    return B, N, H, D, -(-N // block)
+
+
+def _check_attn(q, k, v, block, rowptr, cols):
+    B, N, H, D, nb = _attn_shape(q, block)
+    for t in (q, k, v):
+        _need(t.shape == q.shape and t.dtype == torch.bfloat16, "q, k, v: bf16 [B,N,H,D], same shape")
+    _need(rowptr.dtype == torch.int32 and rowptr.numel() >= B * H * nb + 1, "rowptr int32 [B*H*Nq+1]")
+    _need(cols.dtype == torch.int32, "cols int32")
+    return B, N, H, D, nb
+
+
+def ut_bsattn_fwd(q, k, v, o, lse, block: int, q_rowptr, q_cols, softmax_scale: float,
+                  stream=None) -> int:
+    B, N, H, D, nb = _check_attn(q, k, v, block, q_rowptr, q_cols)
+    _need(o.shape == q.shape and o.dtype == torch.bfloat16, "o: bf16 [B,N,H,D]")
+    _need(lse.dtype == torch.float32 and lse.numel() >= B * H * N, "lse: fp32 [B,H,N]")
+    return lib().ut_bsattn_fwd(_p(q), _p(k), _p(v), _p(o), _p(lse), B, N, H, D, block,
+                               _p(q_rowptr), _p(q_cols), softmax_scale, _stream(stream))
+
+
+def ut_bsattn_bwd_workspace_size(B: int, N: int, H: int) -> int:
+    return int(lib().ut_bsattn_bwd_workspace_size(B, N, H))
+
+
+def ut_bsattn_bwd(q, k, v, o, dout, lse, dq, dk, dv, block: int, q_rowptr, q_cols, kv_colptr,
+                  kv_rows, softmax_scale: float, workspace, stream=None) -> int:
+    B, N, H, D, nb = _check_attn(q, k, v, block, q_rowptr, q_cols)
+    for t in (o, dout, dq, dk, dv):
+        _need(t.shape == q.shape and t.dtype == torch.bfloat16, "o, dout, dq, dk, dv: bf16 [B,N,H,D]")
+    _need(lse.dtype == torch.float32 and lse.numel() >= B * H * N, "lse: fp32 [B,H,N]")
+    _need(kv_colptr.dtype == torch.int32 and kv_colptr.numel() >= B * H * nb + 1, "kv_colptr int32")
+    _need(kv_rows.dtype == torch.int32, "kv_rows int32")
+    ws_bytes = _nbytes(workspace) if workspace is not None else 0
+    return lib().ut_bsattn_bwd(_p(q), _p(k), _p(v), _p(o), _p(dout), _p(lse), _p(dq), _p(dk), _p(dv),
+                               B, N, H, D, block, _p(q_rowptr), _p(q_cols), _p(kv_colptr),
+                               _p(kv_rows), softmax_scale, _p(workspace), ws_bytes, _stream(stream))
+
+
+# ---------------------------------------------------------------------------
+# Allocating helpers (raise on error)
+# ---------------------------------------------------------------------------
+
+def _raise(fn: str, st: int):
+    if st != UT_OK:
+        raise UltraTexError(fn, st, last_error())
+
+
+def drop_background(fg_mask, x_full=None, capacity=None, with_inv=True, stream=None):
+    """Compaction (+ gather when x_full is given). Synchronises once to learn
+    n_kept. Returns dict(kept_idx, inv_idx, n_kept, x_packed)."""
+    dev = fg_mask.device
+    L = fg_mask.numel()
+    cap = L if capacity is None else capacity
+    kept = torch.empty(cap, dtype=torch.int32, device=dev)
+    inv = torch.empty(L, dtype=torch.int32, device=dev) if with_inv else None
+    n_dev = torch.empty(1, dtype=torch.int32, device=dev)
+    ws = torch.empty(max(ut_drop_background_workspace_size(L), 4), dtype=torch.uint8, device=dev)
+    packed = None
+    if x_full is not None:
+        packed = torch.empty((cap,) + tuple(x_full.shape[1:]), dtype=x_full.dtype, device=dev)
+    st, n = ut_drop_background(fg_mask, x_full, packed, kept, inv, n_dev, ws, n_kept_host=True,
+                               stream=stream)
+    _raise("ut_drop_background", st)
+    return {"kept_idx": kept[:n], "inv_idx": inv, "n_kept": n,
+            "x_packed": packed[:n] if packed is not None else None}
+
+
+def scatter_foreground(x_packed, kept_idx, x_full, stream=None):
+    """In place: x_full[kept_idx[k]] = x_packed[k]."""
+    _raise("ut_scatter_foreground",
+           ut_scatter_foreground(x_packed, kept_idx, kept_idx.numel(), x_full, stream))
+    return x_full
+
+
+def build_block_index(block_mask, stream=None):
+    """Row and column lists of a block mask. Synchronises once to learn nnz."""
+    B, H, Nq, Nk = block_mask.shape
+    dev = block_mask.device
+    cap = int(B * H * Nq * Nk)
+    rowptr = torch.empty(B * H * Nq + 1, dtype=torch.int32, device=dev)
+    colptr = torch.empty(B * H * Nk + 1, dtype=torch.int32, device=dev)
+    cols = torch.empty(max(cap, 1), dtype=torch.int32, device=dev)
+    rows = torch.empty(max(cap, 1), dtype=torch.int32, device=dev)
+    st, nnz = ut_build_block_index(block_mask, rowptr, cols, colptr, rows, nnz_host=True,
+                                   stream=stream)
+    _raise("ut_build_block_index", st)
+    return {"q_rowptr": rowptr, "q_cols": cols[:max(nnz, 1)], "kv_colptr": colptr,
+            "kv_rows": rows[:max(nnz, 1)], "nnz": nnz}
+
+
+def bsattn_fwd(q, k, v, index, block: int, softmax_scale: float, stream=None):
+    B, N, H, D = q.shape
+    o = torch.empty_like(q)
+    lse = torch.empty((B, H, N), dtype=torch.float32, device=q.device)
+    _raise("ut_bsattn_fwd", ut_bsattn_fwd(q, k, v, o, lse, block, index["q_rowptr"],
+                                          index["q_cols"], softmax_scale, stream))
+    return o, lse
+
+
+def bsattn_bwd(q, k, v, o, dout, lse, index, block: int, softmax_scale: float, workspace=None,
+               stream=None):
+    B, N, H, D = q.shape
+    dq, dk, dv = torch.empty_like(q), torch.empty_like(q), torch.empty_like(q)
+    if workspace is None:
+        workspace = torch.empty(ut_bsattn_bwd_workspace_size(B, N, H), dtype=torch.uint8,
+                                device=q.device)
+    _raise("ut_bsattn_bwd", ut_bsattn_bwd(q, k, v, o, dout, lse, dq, dk, dv, block,
+                                          index["q_rowptr"], index["q_cols"], index["kv_colptr"],
+                                          index["kv_rows"], softmax_scale, workspace, stream))
+    return dq, dk, dv

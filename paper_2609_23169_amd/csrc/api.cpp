@@ -1,0 +1,227 @@
+// Host side of the C ABI declared in include/ultratex.h: argument validation,
+// workspace sizing, status codes and the per-thread error message. Every
+// check runs before any launch; no exception leaves this file.
+#include <cmath>
+#include <cstdarg>
+#include <cstdio>
+#include <cstring>
+
+#include "common.h"
+
+namespace ut {
+namespace {
+thread_local char g_last_error[512] = "";
+
+bool aligned(const void* p, uintptr_t a) { return (reinterpret_cast<uintptr_t>(p) % a) == 0; }
+}  // namespace
+
+ut_status fail(ut_status st, const char* fmt, ...) {
+  va_list ap;
+  va_start(ap, fmt);
+  vsnprintf(g_last_error, sizeof(g_last_error), fmt, ap);
+  va_end(ap);
+  return st;
+}
+
+ut_status check_hip(hipError_t e, const char* what) {
+  if (e == hipSuccess) return UT_OK;
+  return fail(UT_ERR_HIP, "%s: %s", what, hipGetErrorString(e));
+}
+
+namespace {
+
+ut_status check_attn_common(const char* fn, int32_t B, int32_t N, int32_t H, int32_t D,
+                            int32_t block, float scale) {
+  if (B < 1 || N < 1 || H < 1)
+    return fail(UT_ERR_INVALID_ARG, "%s: B, N, H must be >= 1 (got %d, %d, %d)", fn, B, N, H);
+  if (D != 64 && D != 128)
+    return fail(UT_ERR_UNSUPPORTED, "%s: head_dim %d unsupported (64 or 128)", fn, D);
+  if (block != 64 && block != 128)
+    return fail(UT_ERR_UNSUPPORTED, "%s: block %d unsupported (64 or 128)", fn, block);
+  if (!std::isfinite(scale))
+    return fail(UT_ERR_INVALID_ARG, "%s: softmax_scale must be finite", fn);
+  const int64_t nblk = (N + block - 1) / block;
+  if ((int64_t)B * H * nblk >= (int64_t)1 << 31 || (int64_t)B * N * H * D >= (int64_t)1 << 40)
+    return fail(UT_ERR_INVALID_ARG, "%s: problem too large", fn);
+  return UT_OK;
+}
+
+ut_status check_ptr(const char* fn, const char* name, const void* p, uintptr_t align) {
+  if (!p) return fail(UT_ERR_INVALID_ARG, "%s: %s is NULL", fn, name);
+  if (!aligned(p, align))
+    return fail(UT_ERR_INVALID_ARG, "%s: %s must be %zu-byte aligned", fn, name, (size_t)align);
+  return UT_OK;
+}
+
+#define UT_TRY(x)                     \
+  do {                                \
+    ut_status _s = (x);               \
+    if (_s != UT_OK) return _s;       \
+  } while (0)
+
+}  // namespace
+}  // namespace ut
+
+using namespace ut;
+
+extern "C" {
+
+const char* ut_last_error(void) { return g_last_error; }
+
+int ut_abi_version(void) { return UT_ABI_VERSION; }
+
+size_t ut_drop_background_workspace_size(int64_t L) {
+  if (L < 1) return 0;
+  return (size_t)compact_tiles(L) * sizeof(int32_t);
+}
+
+ut_status ut_drop_background(const uint8_t* fg_mask, int64_t L, const void* x_full,
+                             int64_t row_bytes, void* x_packed, int64_t capacity,
+                             int32_t* kept_idx, int32_t* inv_idx, int32_t* n_kept,
+                             int64_t* n_kept_host, void* workspace, size_t workspace_bytes,
+                             hipStream_t stream) {
+  static const char* fn = "ut_drop_background";
+  g_last_error[0] = 0;
+  if (L < 1 || L >= ((int64_t)1 << 31))
+    return fail(UT_ERR_INVALID_ARG, "%s: L must be in [1, 2^31) (got %lld)", fn, (long long)L);
+  if (capacity < 0) return fail(UT_ERR_INVALID_ARG, "%s: capacity < 0", fn);
+  UT_TRY(check_ptr(fn, "fg_mask", fg_mask, 1));
+  UT_TRY(check_ptr(fn, "n_kept", n_kept, 4));
+  if (capacity > 0) UT_TRY(check_ptr(fn, "kept_idx", kept_idx, 4));
+  if (inv_idx) UT_TRY(check_ptr(fn, "inv_idx", inv_idx, 4));
+  if ((x_full == nullptr) != (x_packed == nullptr))
+    return fail(UT_ERR_INVALID_ARG, "%s: x_full and x_packed must both be NULL or both set", fn);
+  if (x_full) {
+    if (row_bytes <= 0 || row_bytes % 16 != 0)
+      return fail(UT_ERR_INVALID_ARG, "%s: row_bytes must be a positive multiple of 16 (got %lld)",
+                  fn, (long long)row_bytes);
+    UT_TRY(check_ptr(fn, "x_full", x_full, 16));
+    UT_TRY(check_ptr(fn, "x_packed", x_packed, 16));
+  }
+  const size_t need = ut_drop_background_workspace_size(L);
+  if (!workspace || workspace_bytes < need)
+    return fail(UT_ERR_WORKSPACE, "%s: workspace of %zu bytes required (got %zu)", fn, need,
+                workspace ? workspace_bytes : (size_t)0);
+  UT_TRY(check_ptr(fn, "workspace", workspace, 4));
+
+  UT_TRY(check_hip(launch_compact(fg_mask, L, capacity, kept_idx, inv_idx, n_kept,
+                                  static_cast<int32_t*>(workspace), stream),
+                   "compaction launch"));
+  if (x_full)
+    UT_TRY(check_hip(launch_gather(x_full, row_bytes, x_packed, capacity, kept_idx, n_kept, stream),
+                     "gather launch"));
+  if (n_kept_host) {
+    int32_t n = 0;
+    UT_TRY(check_hip(hipMemcpyAsync(&n, n_kept, sizeof(n), hipMemcpyDeviceToHost, stream),
+                     "n_kept copy"));
+    UT_TRY(check_hip(hipStreamSynchronize(stream), "stream sync"));
+    *n_kept_host = n;
+    if (n > capacity)
+      return fail(UT_ERR_CAPACITY, "%s: %d kept positions exceed capacity %lld", fn, n,
+                  (long long)capacity);
+  }
+  return UT_OK;
+}
+
+ut_status ut_scatter_foreground(const void* x_packed, const int32_t* kept_idx, int64_t n_kept,
+                                int64_t row_bytes, void* x_full, hipStream_t stream) {
+  static const char* fn = "ut_scatter_foreground";
+  g_last_error[0] = 0;
+  if (n_kept < 0 || n_kept >= ((int64_t)1 << 31))
+    return fail(UT_ERR_INVALID_ARG, "%s: n_kept out of range", fn);
+  if (row_bytes <= 0 || row_bytes % 16 != 0)
+    return fail(UT_ERR_INVALID_ARG, "%s: row_bytes must be a positive multiple of 16", fn);
+  if (n_kept == 0) return UT_OK;
+  UT_TRY(check_ptr(fn, "x_packed", x_packed, 16));
+  UT_TRY(check_ptr(fn, "x_full", x_full, 16));
+  UT_TRY(check_ptr(fn, "kept_idx", kept_idx, 4));
+  return check_hip(launch_scatter(x_packed, kept_idx, n_kept, row_bytes, x_full, stream),
+                   "scatter launch");
+}
+
+ut_status ut_build_block_index(const uint8_t* block_mask, int32_t B, int32_t H, int32_t Nq,
+                               int32_t Nk, int32_t* q_rowptr, int32_t* q_cols,
+                               int32_t* kv_colptr, int32_t* kv_rows, int64_t cap,
+                               int64_t* nnz_host, hipStream_t stream) {
+  static const char* fn = "ut_build_block_index";
+  g_last_error[0] = 0;
+  if (B < 1 || H < 1 || Nq < 1 || Nk < 1)
+    return fail(UT_ERR_INVALID_ARG, "%s: B, H, Nq, Nk must be >= 1", fn);
+  if ((int64_t)B * H > 65535 || (int64_t)B * H * (Nq > Nk ? Nq : Nk) >= ((int64_t)1 << 31))
+    return fail(UT_ERR_INVALID_ARG, "%s: problem too large", fn);
+  if (cap < 0) return fail(UT_ERR_INVALID_ARG, "%s: cap < 0", fn);
+  UT_TRY(check_ptr(fn, "block_mask", block_mask, 1));
+  UT_TRY(check_ptr(fn, "q_rowptr", q_rowptr, 4));
+  UT_TRY(check_ptr(fn, "kv_colptr", kv_colptr, 4));
+  if (cap > 0) {
+    UT_TRY(check_ptr(fn, "q_cols", q_cols, 4));
+    UT_TRY(check_ptr(fn, "kv_rows", kv_rows, 4));
+  }
+  UT_TRY(check_hip(launch_block_index(block_mask, B, H, Nq, Nk, q_rowptr, q_cols, kv_colptr,
+                                      kv_rows, cap, stream),
+                   "block index launch"));
+  if (nnz_host) {
+    int32_t nnz = 0;
+    UT_TRY(check_hip(hipMemcpyAsync(&nnz, q_rowptr + (int64_t)B * H * Nq, sizeof(nnz),
+                                    hipMemcpyDeviceToHost, stream),
+                     "nnz copy"));
+    UT_TRY(check_hip(hipStreamSynchronize(stream), "stream sync"));
+    *nnz_host = nnz;
+    if (nnz > cap)
+      return fail(UT_ERR_CAPACITY, "%s: %d retained pairs exceed cap %lld", fn, nnz,
+                  (long long)cap);
+  }
+  return UT_OK;
+}
+
+ut_status ut_bsattn_fwd(const void* q, const void* k, const void* v, void* o, float* lse,
+                        int32_t B, int32_t N, int32_t H, int32_t D, int32_t block,
+                        const int32_t* q_rowptr, const int32_t* q_cols, float softmax_scale,
+                        hipStream_t stream) {
+  static const char* fn = "ut_bsattn_fwd";
+  g_last_error[0] = 0;
+  UT_TRY(check_attn_common(fn, B, N, H, D, block, softmax_scale));
+  UT_TRY(check_ptr(fn, "q", q, 16));
+  UT_TRY(check_ptr(fn, "k", k, 16));
+  UT_TRY(check_ptr(fn, "v", v, 16));
+  UT_TRY(check_ptr(fn, "o", o, 16));
+  UT_TRY(check_ptr(fn, "lse", lse, 4));
+  UT_TRY(check_ptr(fn, "q_rowptr", q_rowptr, 4));
+  UT_TRY(check_ptr(fn, "q_cols", q_cols, 4));
+  const AttnShape sh{B, N, H, D, block, (N + block - 1) / block, softmax_scale};
+  return check_hip(launch_bsattn_fwd(q, k, v, o, lse, sh, q_rowptr, q_cols, stream),
+                   "forward launch");
+}
+
+size_t ut_bsattn_bwd_workspace_size(int32_t B, int32_t N, int32_t H) {
+  if (B < 1 || N < 1 || H < 1) return 0;
+  return (size_t)B * H * N * sizeof(float);
+}
+
+ut_status ut_bsattn_bwd(const void* q, const void* k, const void* v, const void* o,
+                        const void* dout, const float* lse, void* dq, void* dk, void* dv,
+                        int32_t B, int32_t N, int32_t H, int32_t D, int32_t block,
+                        const int32_t* q_rowptr, const int32_t* q_cols,
+                        const int32_t* kv_colptr, const int32_t* kv_rows, float softmax_scale,
+                        void* workspace, size_t workspace_bytes, hipStream_t stream) {
+  static const char* fn = "ut_bsattn_bwd";
+  g_last_error[0] = 0;
+  UT_TRY(check_attn_common(fn, B, N, H, D, block, softmax_scale));
+  const struct { const char* n; const void* p; uintptr_t a; } ptrs[] = {
+      {"q", q, 16},   {"k", k, 16},   {"v", v, 16},         {"o", o, 16},
+      {"dout", dout, 16}, {"lse", lse, 4}, {"dq", dq, 16},   {"dk", dk, 16},
+      {"dv", dv, 16}, {"q_rowptr", q_rowptr, 4}, {"q_cols", q_cols, 4},
+      {"kv_colptr", kv_colptr, 4}, {"kv_rows", kv_rows, 4}};
+  for (const auto& p : ptrs) UT_TRY(check_ptr(fn, p.n, p.p, p.a));
+  const size_t need = ut_bsattn_bwd_workspace_size(B, N, H);
+  if (!workspace || workspace_bytes < need)
+    return fail(UT_ERR_WORKSPACE, "%s: workspace of %zu bytes required (got %zu)", fn, need,
+                workspace ? workspace_bytes : (size_t)0);
+  UT_TRY(check_ptr(fn, "workspace", workspace, 16));
+  const AttnShape sh{B, N, H, D, block, (N + block - 1) / block, softmax_scale};
+  return check_hip(launch_bsattn_bwd(q, k, v, o, dout, lse, dq, dk, dv, sh, q_rowptr, q_cols,
+                                     kv_colptr, kv_rows, static_cast<float*>(workspace), stream),
+                   "backward launch");
+}
+
+}  // extern "C"

@@ -1,0 +1,65 @@
+// Device helpers shared by the attention kernels (gfx950, wave64).
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace ut {
+
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef __bf16 bf16x4 __attribute__((ext_vector_type(4)));
+typedef float f32x16 __attribute__((ext_vector_type(16)));
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+typedef short s16x4 __attribute__((ext_vector_type(4)));
+typedef short s16x8 __attribute__((ext_vector_type(8)));
+typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
+
+typedef __attribute__((address_space(3))) s16x4 lds_s16x4;
+
+// D = A(32x16) * B(16x32) + C. Lane l holds A[l%32][8(l/32)+e], B[8(l/32)+e][l%32]
+// (e = 0..7) and C[8(i/4) + 4(l/32) + i%4][l%32] (i = 0..15).
+__device__ inline f32x16 mfma32(bf16x8 a, bf16x8 b, f32x16 c) {
+  return __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, b, c, 0, 0, 0);
+}
+
+// Transposing LDS read: in each 16-lane group, lanes 4r..4r+3 address row r
+// (four consecutive 16-bit elements each); lane j receives element j of the
+// 16-element rows r = 0..3.
+__device__ inline s16x4 lds_read_tr16(const void* p) {
+  return __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_s16x4*)(p));
+}
+
+// Value of lane l ^ 32 combined with this lane's (both halves get the result).
+__device__ inline float pair_max(float x) {
+  const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+  return fmaxf(__uint_as_float(r[0]), __uint_as_float(r[1]));
+}
+__device__ inline float pair_sum(float x) {
+  const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+  return __uint_as_float(r[0]) + __uint_as_float(r[1]);
+}
+
+__device__ inline float fast_exp2(float x) { return __builtin_amdgcn_exp2f(x); }
+
+// LDS byte offset of logical 16-byte chunk c of row r in a tile of CPR chunks
+// per row. The XOR swizzle makes both access patterns conflict-free: 32-row
+// b128 reads of one chunk (the swizzle is injective over 16 consecutive rows)
+// and transposing 8-byte reads of 4 consecutive rows x 4 chunks (those rows
+// differ in the swizzle's upper two bits).
+template <int CPR>
+__device__ inline int lds_off(int r, int c) {
+  static_assert(CPR == 16 || CPR == 8, "rows of 128 or 64 bf16");
+  const int sw = CPR == 16 ? (((r & 3) << 2) | ((r >> 2) & 3)) : ((r >> 1) & 7);
+  return r * CPR * 16 + ((c ^ sw) << 4);
+}
+
+// Workgroups are dispatched round-robin over the 8 XCDs (workgroup w runs on
+// XCD w % 8). Renumber so each XCD receives one contiguous range of logical
+// tiles: neighbouring query blocks of one head then share that XCD's L2.
+__device__ inline int64_t xcd_tile(int64_t w, int64_t G) {
+  const int64_t xcd = w % 8, slot = w / 8;
+  const int64_t per = G / 8, rem = G % 8;
+  return xcd * per + (xcd < rem ? xcd : rem) + slot;
+}
+
+}  // namespace ut

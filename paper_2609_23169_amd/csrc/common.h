@@ -1,0 +1,46 @@
+// Internal declarations shared by the HIP sources of libultratex.so.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include "ultratex.h"
+
+namespace ut {
+
+// Records a message for ut_last_error() and returns `st`.
+ut_status fail(ut_status st, const char* fmt, ...);
+// Maps a HIP error (if any) to UT_ERR_HIP with context; UT_OK otherwise.
+ut_status check_hip(hipError_t e, const char* what);
+
+// ---- Background Token Dropping (btd.hip) ----
+constexpr int kCompactTile = 4096;   // mask bytes per workgroup of the scan
+int64_t compact_tiles(int64_t L);
+hipError_t launch_compact(const uint8_t* mask, int64_t L, int64_t capacity, int32_t* kept_idx,
+                          int32_t* inv_idx, int32_t* n_kept, int32_t* tile_scratch,
+                          hipStream_t s);
+hipError_t launch_gather(const void* x_full, int64_t row_bytes, void* x_packed, int64_t capacity,
+                         const int32_t* kept_idx, const int32_t* n_kept, hipStream_t s);
+hipError_t launch_scatter(const void* x_packed, const int32_t* kept_idx, int64_t n_kept,
+                          int64_t row_bytes, void* x_full, hipStream_t s);
+
+// ---- Block index (block_index.hip) ----
+hipError_t launch_block_index(const uint8_t* mask, int B, int H, int Nq, int Nk,
+                              int32_t* q_rowptr, int32_t* q_cols, int32_t* kv_colptr,
+                              int32_t* kv_rows, int64_t cap, hipStream_t s);
+
+// ---- Attention (bsattn_fwd.hip, bsattn_bwd.hip) ----
+struct AttnShape {
+  int B, N, H, D, block, nblk;
+  float scale;
+};
+hipError_t launch_bsattn_fwd(const void* q, const void* k, const void* v, void* o, float* lse,
+                             const AttnShape& sh, const int32_t* rowptr, const int32_t* cols,
+                             hipStream_t s);
+hipError_t launch_bsattn_bwd(const void* q, const void* k, const void* v, const void* o,
+                             const void* dout, const float* lse, void* dq, void* dk, void* dv,
+                             const AttnShape& sh, const int32_t* rowptr, const int32_t* cols,
+                             const int32_t* colptr, const int32_t* rows, float* delta,
+                             hipStream_t s);
+
+}  // namespace ut

@@ -1,0 +1,113 @@
+"""The C-ABI library loads, exports every declared symbol, and rejects bad
+arguments on the host before any launch (no GPU needed for these paths)."""
+import ctypes
+import os
+import re
+
+import pytest
+
+import paper_2609_23169_amd as ut
+
+HEADER = os.path.join(os.path.dirname(os.path.dirname(os.path.abspath(__file__))), "include",
+                      "ultratex.h")
+
+FAKE = ctypes.c_void_p(0x10000)        # aligned, never dereferenced on these paths
+MISALIGNED = ctypes.c_void_p(0x10002)
+
+
+def declared_functions():
+    text = open(HEADER).read()
+    return sorted(set(re.findall(r"\b(ut_[a-z_0-9]+)\s*\(", text)))
+
+
+def test_header_and_binding_agree():
+    assert declared_functions() == sorted(ut.EXPORTS)
+
+
+def test_library_exports_every_declared_symbol():
+    lib = ut.lib()
+    for name in declared_functions():
+        assert hasattr(lib, name), name
+    assert lib.ut_abi_version() == 1
+
+
+def test_workspace_sizes():
+    assert ut.ut_drop_background_workspace_size(212992) == 52 * 4
+    assert ut.ut_drop_background_workspace_size(1) == 4
+    assert ut.ut_drop_background_workspace_size(0) == 0
+    assert ut.ut_bsattn_bwd_workspace_size(1, 77586, 24) == 77586 * 24 * 4
+
+
+def _fwd(**kw):
+    a = dict(q=FAKE, k=FAKE, v=FAKE, o=FAKE, lse=FAKE, B=1, N=100, H=2, D=128, block=128,
+             rowptr=FAKE, cols=FAKE, scale=0.1)
+    a.update(kw)
+    return ut.lib().ut_bsattn_fwd(a["q"], a["k"], a["v"], a["o"], a["lse"], a["B"], a["N"], a["H"],
+                                  a["D"], a["block"], a["rowptr"], a["cols"], a["scale"], None)
+
+
+@pytest.mark.parametrize("kw,status,msg", [
+    (dict(D=96), ut.UT_ERR_UNSUPPORTED, "head_dim"),
+    (dict(block=32), ut.UT_ERR_UNSUPPORTED, "block"),
+    (dict(N=0), ut.UT_ERR_INVALID_ARG, "must be >= 1"),
+    (dict(H=0), ut.UT_ERR_INVALID_ARG, "must be >= 1"),
+    (dict(q=None), ut.UT_ERR_INVALID_ARG, "q is NULL"),
+    (dict(v=MISALIGNED), ut.UT_ERR_INVALID_ARG, "aligned"),
+    (dict(cols=None), ut.UT_ERR_INVALID_ARG, "q_cols is NULL"),
+    (dict(scale=float("nan")), ut.UT_ERR_INVALID_ARG, "finite"),
+])
+def test_fwd_rejects_bad_arguments(kw, status, msg):
+    assert _fwd(**kw) == status
+    assert msg in ut.last_error()
+
+
+def test_bwd_rejects_missing_workspace():
+    lib = ut.lib()
+    args = [FAKE] * 9 + [1, 100, 2, 128, 128] + [FAKE] * 4 + [0.1]
+    st = lib.ut_bsattn_bwd(*args, None, 0, None)
+    assert st == ut.UT_ERR_WORKSPACE and "workspace" in ut.last_error()
+    st = lib.ut_bsattn_bwd(*args, FAKE, 100 * 2 * 4 - 4, None)
+    assert st == ut.UT_ERR_WORKSPACE
+    args[2] = None
+    assert lib.ut_bsattn_bwd(*args, FAKE, 800, None) == ut.UT_ERR_INVALID_ARG
+
+
+def test_drop_background_rejects_bad_arguments():
+    lib = ut.lib()
+    ws = ut.ut_drop_background_workspace_size(1000)
+    call = lambda **kw: lib.ut_drop_background(
+        kw.get("mask", FAKE), kw.get("L", 1000), kw.get("xf", FAKE), kw.get("rb", 6144),
+        kw.get("xp", FAKE), kw.get("cap", 1000), kw.get("kept", FAKE), kw.get("inv", None),
+        kw.get("n", FAKE), None, kw.get("ws", FAKE), kw.get("wsb", ws), None)
+    assert call(L=0) == ut.UT_ERR_INVALID_ARG
+    assert call(L=1 << 31) == ut.UT_ERR_INVALID_ARG
+    assert call(rb=100) == ut.UT_ERR_INVALID_ARG and "multiple of 16" in ut.last_error()
+    assert call(xp=None) == ut.UT_ERR_INVALID_ARG
+    assert call(xf=MISALIGNED) == ut.UT_ERR_INVALID_ARG
+    assert call(mask=None) == ut.UT_ERR_INVALID_ARG
+    assert call(cap=-1) == ut.UT_ERR_INVALID_ARG
+    assert call(wsb=ws - 1) == ut.UT_ERR_WORKSPACE
+    assert call(ws=None) == ut.UT_ERR_WORKSPACE
+
+
+def test_scatter_and_block_index_reject_bad_arguments():
+    lib = ut.lib()
+    assert lib.ut_scatter_foreground(FAKE, FAKE, 10, 24, FAKE, None) == ut.UT_ERR_INVALID_ARG
+    assert lib.ut_scatter_foreground(FAKE, FAKE, -1, 32, FAKE, None) == ut.UT_ERR_INVALID_ARG
+    assert lib.ut_scatter_foreground(None, None, 0, 32, None, None) == ut.UT_OK   # no-op
+    assert lib.ut_scatter_foreground(FAKE, FAKE, 10, 32, MISALIGNED, None) == ut.UT_ERR_INVALID_ARG
+    bi = lambda B=1, H=2, Nq=5, Nk=5, mask=FAKE, rp=FAKE, cap=50: lib.ut_build_block_index(
+        mask, B, H, Nq, Nk, rp, FAKE, FAKE, FAKE, cap, None, None)
+    assert bi(Nq=0) == ut.UT_ERR_INVALID_ARG
+    assert bi(mask=None) == ut.UT_ERR_INVALID_ARG
+    assert bi(rp=MISALIGNED) == ut.UT_ERR_INVALID_ARG
+    assert bi(cap=-1) == ut.UT_ERR_INVALID_ARG
+    assert bi(B=300, H=300) == ut.UT_ERR_INVALID_ARG
+
+
+def test_binding_refuses_host_tensors():
+    import torch
+    q = torch.zeros((1, 64, 1, 64), dtype=torch.bfloat16)
+    idx = torch.zeros(2, dtype=torch.int32)
+    with pytest.raises(ValueError):
+        ut.ut_bsattn_fwd(q, q, q, q, torch.zeros(64), 64, idx, idx, 0.125)
