@@ -1,0 +1,212 @@
+"""Benchmark of UltraTex's foreground hot path on one MI355X.
+
+One step = one pass of the whole path over one synthetic 2048-canvas
+multi-view sequence (212,992 tokens, 13 views of 128 x 128):
+  1. Background Token Dropping: mask compaction + gather of the
+     212,992 x 3072 bf16 hidden state (ut_drop_background);
+  2. block lists from the block mask (ut_build_block_index);
+  3. block-sparse attention forward (ut_bsattn_fwd) and
+  4. backward (ut_bsattn_bwd), 24 heads x 128, block 128;
+  5. write-back of the packed rows (ut_scatter_foreground).
+Inputs are resident in HBM before the timed region.
+
+`value` is effective TFLOP/s: the algorithmic FLOPs of attention forward +
+backward over retained block pairs only (forward 4 r c d per pair, backward
+2.5x that) divided by the time of the whole step. The roofline object is the
+forward kernel's, timed with HIP events on the stream it runs on.
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import math
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+PEAK_BF16_TFLOPS = 2516.6     # MI355X dense bf16 MFMA (256 CU x 2.4 GHz x 4096 FLOP/clk)
+PEAK_HBM_GBS = 8000.0
+
+
+def parse():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--workload", default="c2k_train")
+    ap.add_argument("--rho", default="0.1")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--cpu-seconds", type=float, default=12.0,
+                    help="CPU time budget of the oracle baseline sample")
+    return ap.parse_args()
+
+
+def cpu_baseline(inst, budget_s: float) -> dict:
+    """The float64 oracle timed on this host on a bounded sample: all query
+    blocks of head 0 in order, forward + backward, until the budget is used."""
+    import numpy as np
+    import oracle
+    import workloads as W
+    wl = inst.wl
+    n, blk = inst.n_kept, wl.block
+    sl = lambda t: t[:, :, :1, :].contiguous()
+    q, k, v, do = sl(inst.q), sl(inst.k), sl(inst.v), sl(inst.do)
+    bm = inst.block_mask[:, :1]
+    nb = bm.shape[-1]
+    sizes = W.block_sizes(n, blk)
+    done, flops, t0 = 0, 0, time.perf_counter()
+    while done < nb and time.perf_counter() - t0 < budget_s:
+        chunk = list(range(done, min(nb, done + 8)))
+        oracle.bsattn_fwd(q, k, v, bm, blk, 1 / math.sqrt(wl.head_dim), q_blocks=chunk)
+        oracle.bsattn_bwd(q, k, v, do, bm, blk, 1 / math.sqrt(wl.head_dim), q_blocks=chunk)
+        pairs = int(np.einsum("ij,i,j->", bm[0, 0, chunk].astype(np.int64), sizes[chunk], sizes))
+        flops += int(3.5 * 4 * wl.head_dim * pairs)
+        done = chunk[-1] + 1
+    dt = time.perf_counter() - t0
+    try:
+        import threadpoolctl
+        cores = max(i.get("num_threads", 1) for i in threadpoolctl.threadpool_info()) or 1
+    except Exception:
+        cores = os.cpu_count() or 1
+    return {"value": round(flops / dt / 1e12, 6), "unit": "TFLOP/s", "cores": int(cores),
+            "kind": "oracle",
+            "sample": f"float64 oracle forward+backward, head 0 of 24, query blocks 0..{done - 1} "
+                      f"of {nb} ({done / nb / 24:.2%} of the step's attention work), "
+                      f"{dt:.1f} s wall"}
+
+
+def main():
+    args = parse()
+    if args.gpus != 1:
+        print(f"bench.py runs on one GPU; --gpus {args.gpus} is not supported in this build "
+              f"(the path would shard by heads; see the design notes).", file=sys.stderr)
+        sys.exit(2)
+    import numpy as np
+    import torch
+
+    import paper_2609_23169_amd as ut
+    import workloads as W
+
+    wl = W.WORKLOADS[args.workload]
+    if args.rho:
+        wl = wl.with_rho(args.rho)
+    inst = W.make(wl, with_do=True, with_hidden=bool(wl.hidden))
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+    n, H, D, blk = inst.n_kept, wl.heads, wl.head_dim, wl.block
+    scale = 1.0 / math.sqrt(D)
+    nb = -(-n // blk)
+
+    # ---- inputs resident in HBM
+    mask = torch.from_numpy(inst.fg_mask).to(dev)
+    hidden = inst.hidden.to(dev) if inst.hidden is not None else None
+    bm = torch.from_numpy(inst.block_mask).to(dev)
+    q, k, v, do = (t.to(dev) for t in (inst.q, inst.k, inst.v, inst.do))
+    L = wl.seq_len
+    kept = torch.empty(n, dtype=torch.int32, device=dev)
+    n_dev = torch.empty(1, dtype=torch.int32, device=dev)
+    ws_drop = torch.empty(ut.ut_drop_background_workspace_size(L), dtype=torch.uint8, device=dev)
+    packed = torch.empty((n, wl.hidden), dtype=torch.bfloat16, device=dev) if hidden is not None else None
+    full_out = torch.zeros_like(hidden) if hidden is not None else None
+    nnz = int(inst.block_mask.sum())
+    rowptr = torch.empty(H * nb + 1, dtype=torch.int32, device=dev)
+    colptr = torch.empty(H * nb + 1, dtype=torch.int32, device=dev)
+    cols = torch.empty(nnz, dtype=torch.int32, device=dev)
+    rows = torch.empty(nnz, dtype=torch.int32, device=dev)
+    o = torch.empty_like(q)
+    lse = torch.empty((1, H, n), dtype=torch.float32, device=dev)
+    dq, dk, dv = torch.empty_like(q), torch.empty_like(q), torch.empty_like(q)
+    ws_bwd = torch.empty(ut.ut_bsattn_bwd_workspace_size(1, n, H), dtype=torch.uint8, device=dev)
+
+    stream = torch.cuda.current_stream()
+    phases = ["drop", "index", "fwd", "bwd", "scatter"]
+
+    def check(st, fn):
+        if st != ut.UT_OK:
+            raise ut.UltraTexError(fn, st, ut.last_error())
+
+    def step(ev=None):
+        rec = (lambda i: ev[i].record(stream)) if ev else (lambda i: None)
+        rec(0)
+        check(ut.ut_drop_background(mask, hidden, packed, kept, None, n_dev, ws_drop)[0], "drop")
+        rec(1)
+        check(ut.ut_build_block_index(bm, rowptr, cols, colptr, rows)[0], "index")
+        rec(2)
+        check(ut.ut_bsattn_fwd(q, k, v, o, lse, blk, rowptr, cols, scale), "fwd")
+        rec(3)
+        check(ut.ut_bsattn_bwd(q, k, v, o, do, lse, dq, dk, dv, blk, rowptr, cols, colptr, rows,
+                               scale, ws_bwd), "bwd")
+        rec(4)
+        if hidden is not None:
+            check(ut.ut_scatter_foreground(packed, kept, n, full_out), "scatter")
+        rec(5)
+
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+    events = [[torch.cuda.Event(enable_timing=True) for _ in range(6)] for _ in range(args.steps)]
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for s in range(args.steps):
+        step(events[s])
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    per = {p: float(np.mean([events[s][i].elapsed_time(events[s][i + 1]) for s in range(args.steps)]))
+           for i, p in enumerate(phases)}
+    ms_step = wall * 1e3 / args.steps
+
+    fwd_flops = W.retained_flops_fwd(inst.block_mask, n, blk, D)
+    attn_flops = 3.5 * fwd_flops
+    fwd_tflops = fwd_flops / (per["fwd"] * 1e-3) / 1e12
+    bwd_tflops = 2.5 * fwd_flops / (per["bwd"] * 1e-3) / 1e12
+    attn_ms = per["fwd"] + per["bwd"]
+    copy_bytes = 2 * n * wl.hidden * 2 + 4 * n if hidden is not None else 0
+
+    result = {
+        "metric": "block-sparse attn effective TFLOP/s + ms/layer fwd+bwd at 2K (212,992 tok), % MFMA peak",
+        "value": round(attn_flops / (ms_step * 1e-3) / 1e12, 2),
+        "unit": "TFLOP/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms_step, 4),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16",
+        "data": "synthetic",
+        "config": {
+            "workload": f"{wl.name}: {wl.views} views x {wl.grid}x{wl.grid} = {L} tokens, "
+                        f"{n} kept after Background Token Dropping; {H} heads x {D}, block {blk}, "
+                        f"block mask rho={wl.rho} + diagonal ({nnz} retained pairs); attention "
+                        f"forward + backward, gather and scatter of a {L} x {wl.hidden} bf16 state",
+            "seq_len": L, "kept_tokens": n, "heads": H, "head_dim": D, "block": blk, "rho": wl.rho,
+            "retained_pairs": nnz, "parallelism": "single GPU",
+        },
+        "attention": {
+            "ms_per_layer_fwd_bwd": round(attn_ms, 4),
+            "tflops_fwd_bwd": round(attn_flops / (attn_ms * 1e-3) / 1e12, 2),
+            "pct_peak_fwd_bwd": round(100 * attn_flops / (attn_ms * 1e-3) / 1e12 / PEAK_BF16_TFLOPS, 2),
+            "ms_fwd": round(per["fwd"], 4), "tflops_fwd": round(fwd_tflops, 2),
+            "pct_peak_fwd": round(100 * fwd_tflops / PEAK_BF16_TFLOPS, 2),
+            "ms_bwd": round(per["bwd"], 4), "tflops_bwd": round(bwd_tflops, 2),
+            "fwd_flops": fwd_flops,
+        },
+        "phases_ms": {p: round(per[p], 4) for p in phases},
+        "copy": {"bytes_gather": copy_bytes,
+                 "gbs_gather": round(copy_bytes / (per["drop"] * 1e-3) / 1e9, 1) if copy_bytes else None,
+                 "gbs_scatter": round(copy_bytes / (per["scatter"] * 1e-3) / 1e9, 1) if copy_bytes else None},
+        "roofline": {"bound": "mfma", "kernel": "bsattn_fwd_kernel<128,128>",
+                     "achieved": round(fwd_tflops, 2), "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s",
+                     "frac": round(fwd_tflops / PEAK_BF16_TFLOPS, 4), "traffic": None},
+    }
+    if not args.no_cpu_baseline:
+        result["cpu_baseline"] = cpu_baseline(inst, args.cpu_seconds)
+    print(json.dumps(result), flush=True)
+
+
+if __name__ == "__main__":
+    main()
