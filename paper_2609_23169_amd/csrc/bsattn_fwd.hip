@@ -3,15 +3,30 @@
 // with an online softmax over the listed key blocks only; key blocks outside
 // S_i are never read.
 //
-// One workgroup per (b, h, i); BLOCK/32 waves, each owning 32 query rows.
+// One workgroup per (b, h, i); BLOCK/32 waves, each owning 32 query rows;
+// two workgroups share a CU, so each SIMD runs two independent waves.
 // Scores are formed transposed, S^T = K Q^T, with 32x32x16 bf16 MFMA: each
-// lane then holds one query column (16 keys per 32x32 tile), so row max and
-// row sum are in-lane plus one permlane32 swap, and the probabilities feed the
+// lane holds one query column (16 keys per 32x32 tile), so row max and row
+// sum are in-lane plus one permlane32 swap, and the probabilities feed the
 // second product O^T += V^T P^T straight from registers as the B operand.
 // V^T operands come from LDS with the transposing ds_read_b64_tr_b16.
-// Keys stream through LDS in 64-key sub-tiles, double buffered: the global
-// loads of sub-tile t+1 are in flight (in registers) while sub-tile t is
-// computed, then written to the other LDS stage before one barrier.
+//
+// The loop is built to spend as few vector instructions per MFMA as
+// possible, since the vector ALU (softmax) and not the matrix core is the
+// scarce resource at head_dim 128:
+//  * K and V tiles (64 keys) go from global memory straight into LDS with
+//    buffer loads; the tile base lives in the scalar buffer descriptor, so
+//    the per-lane offsets are loop invariant, and rows past N fall outside
+//    the descriptor's range and read as zeros;
+//  * the loop is unrolled by two so that both LDS stages are at constant
+//    offsets: every LDS read address is a precomputed lane offset plus an
+//    immediate;
+//  * the running row max only moves when a new score exceeds it by more
+//    than 2^8 (log2 units), so the O rescale is rare (O and the row sum always
+//    use the same max, so the result is exact in real arithmetic);
+//  * only the sub-tiles of a short last key block run the masking code.
+#include <type_traits>
+
 #include "attn_util.h"
 #include "common.h"
 
@@ -20,6 +35,15 @@ namespace {
 
 constexpr float kLog2e = 1.4426950408889634f;
 constexpr float kLn2 = 0.6931471805599453f;
+constexpr float kRescaleSlack = 8.0f;   // log2 units: p = 2^(s - m) stays <= 256
+constexpr int kRsrcWord3 = 0x00020000;  // raw buffer, 32-bit data format
+
+// One 16-byte-per-lane buffer load straight into LDS: lane L writes at
+// lds + 16 L (lds must be wave-uniform).
+__device__ inline void buffer_load_lds16(__amdgpu_buffer_rsrc_t rs, char* lds, int voffset) {
+  __builtin_amdgcn_raw_ptr_buffer_load_lds(rs, (__attribute__((address_space(3))) void*)lds, 16,
+                                           voffset, 0, 0, 0);
+}
 
 template <int D, int BLOCK>
 struct FwdCfg {
@@ -30,12 +54,11 @@ struct FwdCfg {
   static constexpr int ROWB = D * 2;             // bytes per LDS row
   static constexpr int CPR = D / 8;              // 16-byte chunks per row
   static constexpr int TILEB = KT * ROWB;        // one K or V sub-tile
-  static constexpr int STAGEB = 2 * TILEB;       // K + V
-  static constexpr int LDSB = 2 * STAGEB;        // two stages
-  static constexpr int LPT = 2 * KT * CPR / NT;  // 16-byte loads per thread per stage
+  static constexpr int RPI = 1024 / ROWB;        // rows per direct-load instruction
+  static constexpr int IPW = TILEB / 1024 / NW;  // direct-load instructions per wave per tile
   static constexpr int KS = D / 16;              // k-steps of the score product
   static constexpr int DT = D / 32;              // 32-wide d tiles of O
-  static_assert(2 * KT * CPR % NT == 0, "stage must split evenly over threads");
+  static_assert(TILEB % (1024 * NW) == 0, "tile must split evenly over the waves");
 };
 
 template <int D, int BLOCK>
@@ -44,9 +67,15 @@ __global__ __launch_bounds__(64 * (BLOCK / 32), (BLOCK == 128 || D == 64) ? 2 : 
     __bf16* __restrict__ O, float* __restrict__ LSE, int B, int N, int H, int nblk, float scale,
     const int32_t* __restrict__ rowptr, const int32_t* __restrict__ cols) {
   using C = FwdCfg<D, BLOCK>;
-  __shared__ __attribute__((aligned(16))) char smem[C::LDSB];
+  // Four LDS objects (K and V, two stages each): distinct objects let the
+  // compiler see that a load into one never aliases reads of another.
+  __shared__ __attribute__((aligned(1024))) char k_lds0[C::TILEB];
+  __shared__ __attribute__((aligned(1024))) char k_lds1[C::TILEB];
+  __shared__ __attribute__((aligned(1024))) char v_lds0[C::TILEB];
+  __shared__ __attribute__((aligned(1024))) char v_lds1[C::TILEB];
 
-  const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int w = __builtin_amdgcn_readfirstlane(tid >> 6);   // wave index, uniform
   const int l32 = lane & 31, g = lane >> 5;
   const int64_t G = (int64_t)B * H * nblk;
   const int64_t lt = xcd_tile(blockIdx.x, G);
@@ -62,12 +91,12 @@ __global__ __launch_bounds__(64 * (BLOCK / 32), (BLOCK == 128 || D == 64) ? 2 : 
 
   if (T == 0) {  // empty S_i: O = 0, LSE = -inf
     if (q < N) {
-      uint2 z = make_uint2(0, 0);
+      const bf16x4 z = {};
 #pragma unroll
       for (int dt = 0; dt < C::DT; ++dt)
 #pragma unroll
         for (int a = 0; a < 4; ++a)
-          *reinterpret_cast<uint2*>(O + base_bh + q * tok_stride + 32 * dt + 8 * a + 4 * g) = z;
+          *reinterpret_cast<bf16x4*>(O + base_bh + q * tok_stride + 32 * dt + 8 * a + 4 * g) = z;
       if (g == 0) LSE[bh * N + q] = -INFINITY;
     }
     return;
@@ -81,32 +110,48 @@ __global__ __launch_bounds__(64 * (BLOCK / 32), (BLOCK == 128 || D == 64) ? 2 : 
     for (int ks = 0; ks < C::KS; ++ks) qop[ks] = *reinterpret_cast<const bf16x8*>(qp + 16 * ks);
   }
 
-  // Staging: chunk x = tid + NT*u of the stage; tensor (K/V), row, chunk.
-  u32x4 stg[C::LPT];
-  auto load_stage = [&](int t) __attribute__((always_inline)) {
+  // Loop-invariant lane offsets. Direct loads: lane L of instruction u writes
+  // 16 bytes at dst + 1024 (w IPW + u) + 16 L, i.e. row r, physical chunk
+  // p = L mod CPR, which holds logical chunk p ^ swizzle(r); it reads that
+  // chunk of key row r of the tile.
+  int dma_off[C::IPW];
+#pragma unroll
+  for (int u = 0; u < C::IPW; ++u) {
+    const int r = (w * C::IPW + u) * C::RPI + lane / C::CPR, p = lane % C::CPR;
+    const int c = (lds_off<C::CPR>(r, p) >> 4) & (C::CPR - 1);
+    dma_off[u] = r * (int)(tok_stride * 2) + 16 * c;
+  }
+  // Tile t of X (K or V) into `dst`: descriptor base at the tile's first key,
+  // range ending after the last valid key row (rows past N read zeros).
+  auto load_tile = [&](const __bf16* X, int t, char* dst) __attribute__((always_inline)) {
     const int j = cols[p0 + t / C::SUBS];
     const int key0 = j * BLOCK + (t % C::SUBS) * C::KT;
+    const __bf16* tile = X + base_bh + (int64_t)key0 * tok_stride;
+    // a sub-tile wholly past N (second half of a short last block) gets an
+    // empty range: every load reads zeros and nothing past the tensor is touched
+    const int nrec = key0 < N ? (N - key0 - 1) * (int)(tok_stride * 2) + 2 * D : 0;
+    const __amdgpu_buffer_rsrc_t rs = __builtin_amdgcn_make_buffer_rsrc(
+        const_cast<__bf16*>(tile), (short)0, nrec, kRsrcWord3);
 #pragma unroll
-    for (int u = 0; u < C::LPT; ++u) {
-      const int x = tid + C::NT * u;
-      const int isv = x / (C::KT * C::CPR);
-      const int r = (x / C::CPR) % C::KT, c = x % C::CPR;
-      const int key = min(key0 + r, N - 1);
-      const __bf16* src = (isv ? V : K) + base_bh + (int64_t)key * tok_stride + 8 * c;
-      stg[u] = *reinterpret_cast<const u32x4*>(src);
-    }
+    for (int u = 0; u < C::IPW; ++u)
+      buffer_load_lds16(rs, dst + (w * C::IPW + u) * 1024, dma_off[u]);
   };
-  auto store_stage = [&](int s) __attribute__((always_inline)) {
-    char* st = smem + s * C::STAGEB;
+
+  // LDS lane offsets of the two products (immediates add kt, hh and stage).
+  int koff[C::KS];
 #pragma unroll
-    for (int u = 0; u < C::LPT; ++u) {
-      const int x = tid + C::NT * u;
-      const int isv = x / (C::KT * C::CPR);
-      const int r = (x / C::CPR) % C::KT, c = x % C::CPR;
-      const int off = isv ? C::TILEB + lds_off<C::CPR>(r, c) : lds_off<C::CPR>(r, c);
-      *reinterpret_cast<u32x4*>(st + off) = stg[u];
+  for (int ks = 0; ks < C::KS; ++ks) koff[ks] = lds_off<C::CPR>(l32, 2 * ks + g);
+  const int jr = lane & 15;
+  const int dsub = 16 * ((lane >> 4) & 1) + 4 * (jr & 3);
+  int voff[C::DT][2];
+#pragma unroll
+  for (int dt = 0; dt < C::DT; ++dt)
+#pragma unroll
+    for (int lh = 0; lh < 2; ++lh) {
+      const int r0 = 4 * g + (jr >> 2) + 8 * lh;
+      const int d = 32 * dt + dsub;
+      voff[dt][lh] = lds_off<C::CPR>(r0, d >> 3) + 2 * (d & 7);
     }
-  };
 
   const float c2 = scale * kLog2e;   // scores in log2 units
   f32x16 oacc[C::DT];
@@ -114,53 +159,45 @@ __global__ __launch_bounds__(64 * (BLOCK / 32), (BLOCK == 128 || D == 64) ? 2 : 
   for (int dt = 0; dt < C::DT; ++dt) oacc[dt] = f32x16{};
   float m_run = -INFINITY, l_run = 0.f;
 
-  load_stage(0);
-  store_stage(0);
-  __syncthreads();
-
-  for (int t = 0; t < T; ++t) {
-    const int cur = t & 1;
-    if (t + 1 < T) load_stage(t + 1);
-    const char* kt_lds = smem + cur * C::STAGEB;
-    const char* vt_lds = kt_lds + C::TILEB;
-
-    // ---- S^T = K Q^T over the 64 keys: two 32-key tiles
+  // One sub-tile: S^T = K Q^T, online softmax, O^T += V^T P^T. Rows 32 kt + l32
+  // and 32 kt + 16 hh + r of a tile share the swizzle of rows l32 and r (the
+  // swizzle depends on the row mod 16), so kt and hh are pure immediates.
+  auto step = [&](int t, const char* kt_lds, const char* vt_lds, auto masked)
+      __attribute__((always_inline)) {
     f32x16 s[2] = {f32x16{}, f32x16{}};
 #pragma unroll
     for (int ks = 0; ks < C::KS; ++ks)
 #pragma unroll
       for (int kt = 0; kt < 2; ++kt) {
-        const bf16x8 a = *reinterpret_cast<const bf16x8*>(
-            kt_lds + lds_off<C::CPR>(32 * kt + l32, 2 * ks + g));
-        s[kt] = mfma32(a, qop[ks], s[kt]);
+        const bf16x8 av = *reinterpret_cast<const bf16x8*>(kt_lds + koff[ks] + kt * 32 * C::ROWB);
+        s[kt] = mfma32(av, qop[ks], s[kt]);
       }
-
-    // ---- keys past N (only in a short last block) never count
-    const int j = cols[p0 + t / C::SUBS];
-    const int key0 = j * BLOCK + (t % C::SUBS) * C::KT;
-    if (key0 + C::KT > N) {
+    if constexpr (decltype(masked)::value) {   // keys past N in a short last block
+      const int j = cols[p0 + t / C::SUBS];
+      const int lim = N - (j * BLOCK + (t % C::SUBS) * C::KT);
 #pragma unroll
       for (int kt = 0; kt < 2; ++kt)
 #pragma unroll
-        for (int e = 0; e < 16; ++e) {
-          const int key = key0 + 32 * kt + 8 * (e >> 2) + 4 * g + (e & 3);
-          if (key >= N) s[kt][e] = -INFINITY;
-        }
+        for (int e = 0; e < 16; ++e)
+          s[kt][e] = 32 * kt + 8 * (e >> 2) + 4 * g + (e & 3) >= lim ? -INFINITY : s[kt][e];
     }
-
-    // ---- online softmax (lane owns query l32; its partner lane l^32 the other 16 keys)
-    float mx = -INFINITY;
+    float mx = s[0][0];
 #pragma unroll
     for (int kt = 0; kt < 2; ++kt)
 #pragma unroll
-      for (int e = 0; e < 16; ++e) mx = fmaxf(mx, s[kt][e]);
-    mx = pair_max(mx);
-    const float m_new = fmaxf(m_run, mx * c2);
-    const float m_use = m_new == -INFINITY ? 0.f : m_new;
-    const float alpha = fast_exp2(m_run - m_use);
-    m_run = m_new;
-    float lsum = 0.f;
+      for (int e = (kt == 0 ? 1 : 0); e < 16; ++e) mx = fmaxf(mx, s[kt][e]);
+    mx = pair_max(mx) * c2;
+    if (__ballot(mx > m_run + kRescaleSlack)) {      // rare after the first tile
+      const float m_new = fmaxf(m_run, mx);
+      const float alpha = fast_exp2(m_run - m_new);  // 0 on the first tile
+      l_run *= alpha;
+#pragma unroll
+      for (int dt = 0; dt < C::DT; ++dt) oacc[dt] *= alpha;
+      m_run = m_new;
+    }
+    const float m_use = m_run == -INFINITY ? 0.f : m_run;
     bf16x8 pb[2][2];
+    float lsum = 0.f;
 #pragma unroll
     for (int kt = 0; kt < 2; ++kt)
 #pragma unroll
@@ -169,36 +206,72 @@ __global__ __launch_bounds__(64 * (BLOCK / 32), (BLOCK == 128 || D == 64) ? 2 : 
         lsum += p;
         pb[kt][e >> 3][e & 7] = (__bf16)p;
       }
-    l_run = l_run * alpha + lsum;
-    if (__ballot(alpha != 1.f)) {
+    l_run += lsum;
+    // O^T += V^T P^T: P^T tile kt, half hh covers keys 32kt + 16hh + {4g+0..3, 8+4g+0..3}
 #pragma unroll
-      for (int dt = 0; dt < C::DT; ++dt) oacc[dt] *= alpha;
-    }
+    for (int dt = 0; dt < C::DT; ++dt)
+#pragma unroll
+      for (int kt = 0; kt < 2; ++kt)
+#pragma unroll
+        for (int hh = 0; hh < 2; ++hh) {
+          const char* vb = vt_lds + (32 * kt + 16 * hh) * C::ROWB;
+          const s16x4 lo = lds_read_tr16(vb + voff[dt][0]);
+          const s16x4 hi = lds_read_tr16(vb + voff[dt][1]);
+          const s16x8 v8 = {lo[0], lo[1], lo[2], lo[3], hi[0], hi[1], hi[2], hi[3]};
+          oacc[dt] = mfma32(__builtin_bit_cast(bf16x8, v8), pb[kt][hh], oacc[dt]);
+        }
+  };
 
-    // ---- O^T += V^T P^T: P^T tile kt, half hh covers keys 32kt + 16hh + {4g+0..3, 8+4g+0..3}
-    {
-      const int jr = lane & 15;                       // lane within a 16-lane group
-      const int dsub = 16 * ((lane >> 4) & 1) + 4 * (jr & 3);
-#pragma unroll
-      for (int dt = 0; dt < C::DT; ++dt)
-#pragma unroll
-        for (int kt = 0; kt < 2; ++kt)
-#pragma unroll
-          for (int hh = 0; hh < 2; ++hh) {
-            const int r0 = 32 * kt + 16 * hh + 4 * g + (jr >> 2);
-            const int d = 32 * dt + dsub;
-            const s16x4 lo = lds_read_tr16(vt_lds + lds_off<C::CPR>(r0, d >> 3) + 2 * (d & 7));
-            const s16x4 hi = lds_read_tr16(vt_lds + lds_off<C::CPR>(r0 + 8, d >> 3) + 2 * (d & 7));
-            const s16x8 v8 = {lo[0], lo[1], lo[2], lo[3], hi[0], hi[1], hi[2], hi[3]};
-            oacc[dt] = mfma32(__builtin_bit_cast(bf16x8, v8), pb[kt][hh], oacc[dt]);
-          }
+  // Iteration t: issue the loads of tile t+1 into the other stage (read in
+  // iteration t-1, before the last barrier), compute tile t, wait for the
+  // new tile and barrier.
+  auto iter = [&](int t, auto par, auto masked) __attribute__((always_inline)) {
+    constexpr int P = decltype(par)::value;
+    char* const kc = P ? k_lds1 : k_lds0;
+    char* const vc = P ? v_lds1 : v_lds0;
+    char* const kn = P ? k_lds0 : k_lds1;
+    char* const vn = P ? v_lds0 : v_lds1;
+    if (t + 1 < T) {
+      load_tile(K, t + 1, kn);
+      load_tile(V, t + 1, vn);
     }
-
-    if (t + 1 < T) store_stage(cur ^ 1);
+    step(t, kc, vc, masked);
+    __builtin_amdgcn_s_waitcnt(0);
     __syncthreads();
+  };
+
+  load_tile(K, 0, k_lds0);
+  load_tile(V, 0, v_lds0);
+  __builtin_amdgcn_s_waitcnt(0);
+  __syncthreads();
+
+  // The sub-tiles of a short last key block (always the end of the ascending
+  // list) take the masked path.
+  const bool tail = (N % BLOCK != 0) && cols[p1 - 1] == nblk - 1;
+  const int Tm = tail ? T - C::SUBS : T;
+  using I0 = std::integral_constant<int, 0>;
+  using I1 = std::integral_constant<int, 1>;
+  using F = std::false_type;
+  using Tt = std::true_type;
+  int t = 0;
+  for (; t + 1 < Tm; t += 2) {
+    iter(t, I0{}, F{});
+    iter(t + 1, I1{}, F{});
+  }
+  if (t < Tm) {   // one unmasked step left at parity 0; masked steps continue at parity 1
+    iter(t, I0{}, F{});
+    for (++t; t < T; t += 2) {
+      iter(t, I1{}, Tt{});
+      if (t + 1 < T) iter(t + 1, I0{}, Tt{});
+    }
+  } else {        // masked steps from parity 0
+    for (; t < T; t += 2) {
+      iter(t, I0{}, Tt{});
+      if (t + 1 < T) iter(t + 1, I1{}, Tt{});
+    }
   }
 
-  // ---- epilogue: O = O^T / l, LSE = ln(sum) + max
+  // ---- epilogue: O = O^T / l, LSE = (m + log2 l) ln 2
   const float l_tot = pair_sum(l_run);
   const float inv = l_tot > 0.f ? 1.f / l_tot : 0.f;
   if (q < N) {
