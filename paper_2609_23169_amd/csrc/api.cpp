@@ -195,7 +195,7 @@ ut_status ut_bsattn_fwd(const void* q, const void* k, const void* v, void* o, fl
 
 size_t ut_bsattn_bwd_workspace_size(int32_t B, int32_t N, int32_t H) {
   if (B < 1 || N < 1 || H < 1) return 0;
-  return (size_t)B * H * N * sizeof(float);
+  return (size_t)B * H * N * 2 * sizeof(float);   // {LSE log2 e, delta} per query row
 }
 
 ut_status ut_bsattn_bwd(const void* q, const void* k, const void* v, const void* o,

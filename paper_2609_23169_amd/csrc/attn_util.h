@@ -53,6 +53,21 @@ __device__ inline int lds_off(int r, int c) {
   return r * CPR * 16 + ((c ^ sw) << 4);
 }
 
+constexpr int kRsrcWord3 = 0x00020000;  // raw buffer descriptor, 32-bit data format
+
+// A raw buffer descriptor over `bytes` bytes from `base`; loads past the range
+// read zeros.
+__device__ inline __amdgpu_buffer_rsrc_t buffer_rsrc(const void* base, int bytes) {
+  return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), (short)0, bytes, kRsrcWord3);
+}
+
+// One 16-byte-per-lane buffer load straight into LDS: lane L writes at
+// lds + 16 L (lds must be wave-uniform).
+__device__ inline void buffer_load_lds16(__amdgpu_buffer_rsrc_t rs, char* lds, int voffset) {
+  __builtin_amdgcn_raw_ptr_buffer_load_lds(rs, (__attribute__((address_space(3))) void*)lds, 16,
+                                           voffset, 0, 0, 0);
+}
+
 // Workgroups are dispatched round-robin over the 8 XCDs (workgroup w runs on
 // XCD w % 8). Renumber so each XCD receives one contiguous range of logical
 // tiles: neighbouring query blocks of one head then share that XCD's L2.

@@ -1,20 +1,28 @@
 // Block-sparse attention backward on gfx950: gradients of Eq. 8 (paper
-// Sec. 3.3) with the block mask held constant. Three launches, no atomics:
+// Sec. 3.3) with the block mask held constant. Three launches, no atomics,
+// deterministic:
 //
-//   delta  : delta_r = sum_d dO[r,d] * O[r,d]   (fp32, one pass over O and dO)
-//   dK/dV  : one workgroup per (b, h, key block j), walking the query blocks
-//            that select j (column lists). Each wave owns 32 keys and keeps
-//            its K and V rows as MFMA operands in registers. Per 64-query
-//            sub-tile staged in LDS: S = Q K^T and dP = dO V^T (lane = key
-//            column), P = exp(S - LSE), dS = P (dP - delta), then
-//            dV^T += dO^T P and dK^T += Q^T dS with transposing LDS reads.
-//   dQ     : one workgroup per (b, h, query block i), walking S_i (row
-//            lists). Each wave owns 32 queries (Q and dO rows in registers).
-//            Per 64-key sub-tile: S^T = K Q^T, dP^T = V dO^T (lane = query
-//            column), dS^T, then dQ^T += K^T dS^T.
+//   prep  : per query row, {LSE log2(e), delta = sum_d dO[r,d] O[r,d]} (fp32);
+//   dQ    : one workgroup per (b, h, query block i), walking S_i (row lists).
+//           Each wave owns 32 queries, with its Q and dO rows as MFMA operands
+//           in registers. Per 64-key tile streamed through LDS:
+//           S^T = K Q^T and dP^T = V dO^T (lane = query column),
+//           P = exp(S - LSE), dS^T = P^T o (dP^T - delta), dQ^T += K^T dS^T;
+//   dK/dV : one workgroup per (b, h, key block j), walking the query blocks
+//           that select j (column lists). Waves w and w + BLOCK/32 own the
+//           same 32 keys (K rows in registers, V rows in LDS) and split each 64-row
+//           query tile between them: S = Q K^T and dP = dO V^T (lane = key
+//           column), dV^T += dO^T P and dK^T += Q^T dS with transposing LDS
+//           reads. The two partial sums meet once in LDS at the end.
 //
-// The dQ pass recomputes S and dP rather than accumulating dQ with atomics
-// from the dK/dV pass: the result is deterministic.
+// The dQ pass recomputes S and dP instead of accumulating dQ with atomics
+// from the dK/dV pass. Tiles go from global memory straight into LDS with
+// buffer loads; rows past N are outside the descriptor range and read as
+// zeros. For query rows past N that makes every contribution exactly zero
+// (zero Q and dO rows give dP = 0 and delta = 0, hence dS = 0 and P dO = 0).
+// Keys past N are masked explicitly in the dQ pass (their P would not be 0).
+#include <type_traits>
+
 #include "attn_util.h"
 #include "common.h"
 
@@ -24,13 +32,14 @@ namespace {
 constexpr float kLog2e = 1.4426950408889634f;
 
 // ---------------------------------------------------------------------------
-// delta = rowsum(dO o O)
+// prep: aux[(b H + h) N + n] = {LSE log2 e, rowsum(dO o O)}
 // ---------------------------------------------------------------------------
 template <int D>
-__global__ __launch_bounds__(256) void bwd_delta_kernel(const __bf16* __restrict__ O,
-                                                        const __bf16* __restrict__ dO,
-                                                        float* __restrict__ delta, int B, int N,
-                                                        int H) {
+__global__ __launch_bounds__(256) void bwd_prep_kernel(const __bf16* __restrict__ O,
+                                                       const __bf16* __restrict__ dO,
+                                                       const float* __restrict__ LSE,
+                                                       float2* __restrict__ aux, int B, int N,
+                                                       int H) {
   constexpr int CPR = D / 8;  // lanes per (token, head) row
   const int64_t rows = (int64_t)B * N * H;
   const int64_t gid = (int64_t)blockIdx.x * 256 + threadIdx.x;
@@ -49,198 +58,70 @@ __global__ __launch_bounds__(256) void bwd_delta_kernel(const __bf16* __restrict
     const int h = (int)(row % H);
     const int64_t bn = row / H;
     const int n = (int)(bn % N), b = (int)(bn / N);
-    delta[((int64_t)b * H + h) * N + n] = acc;
+    const int64_t r = ((int64_t)b * H + h) * N + n;
+    aux[r] = make_float2(LSE[r] * kLog2e, acc);
   }
 }
 
-template <int D, int BLOCK>
+template <int D, int BLOCK, int NWAVES>
 struct BwdCfg {
-  static constexpr int NW = BLOCK / 32;
-  static constexpr int NT = 64 * NW;
-  static constexpr int ST = 64;                  // rows per sub-tile
-  static constexpr int SUBS = BLOCK / ST;
+  static constexpr int NT = 64 * NWAVES;
+  static constexpr int ST = 64;                  // rows per streamed tile
+  static constexpr int SUBS = BLOCK / ST;        // tiles per block
+  static constexpr int ROWB = D * 2;
   static constexpr int CPR = D / 8;
-  static constexpr int TILEB = ST * D * 2;       // one 64-row bf16 tile
+  static constexpr int TILEB = ST * ROWB;        // one 64-row bf16 tile
+  static constexpr int RPI = 1024 / ROWB;        // rows per direct-load instruction
+  static constexpr int IPW = TILEB / 1024 / NWAVES;
   static constexpr int KS = D / 16;
   static constexpr int DT = D / 32;
-  static constexpr int LPT = 2 * ST * CPR / NT;  // 16-byte loads per thread per stage
-  static_assert(2 * ST * CPR % NT == 0, "stage must split evenly over threads");
+  static_assert(TILEB % (1024 * NWAVES) == 0, "tile must split evenly over the waves");
 };
 
-// ---------------------------------------------------------------------------
-// dK, dV: key-stationary over the column lists
-// ---------------------------------------------------------------------------
-template <int D, int BLOCK>
-__global__ __launch_bounds__(64 * (BLOCK / 32), 1) void bwd_dkdv_kernel(
-    const __bf16* __restrict__ Q, const __bf16* __restrict__ K, const __bf16* __restrict__ V,
-    const __bf16* __restrict__ dO, const float* __restrict__ LSE, const float* __restrict__ delta,
-    __bf16* __restrict__ dK, __bf16* __restrict__ dV, int B, int N, int H, int nblk, float scale,
-    const int32_t* __restrict__ colptr, const int32_t* __restrict__ rows_list) {
-  using C = BwdCfg<D, BLOCK>;
-  constexpr int STAGEB = 2 * C::TILEB + 2 * C::ST * 4;   // Q, dO, lse2, delta
-  __shared__ __attribute__((aligned(16))) char smem[2 * STAGEB];
-
-  const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
-  const int l32 = lane & 31, g = lane >> 5;
-  const int64_t G = (int64_t)B * H * nblk;
-  const int64_t lt = xcd_tile(blockIdx.x, G);
-  const int j = (int)(lt % nblk);
-  const int64_t bh = lt / nblk;
-  const int h = (int)(bh % H), b = (int)(bh / H);
-  const int64_t tok_stride = (int64_t)H * D;
-  const int64_t base_bh = (int64_t)b * N * tok_stride + (int64_t)h * D;
-
-  const int key = j * BLOCK + 32 * w + l32;  // this lane's key row (column of S)
-  const int p0 = colptr[lt], p1 = colptr[lt + 1];
-  const int T = (p1 - p0) * C::SUBS;
-
-  f32x16 dkt[C::DT], dvt[C::DT];
+// Loop-invariant lane offsets shared by both passes.
+template <class C>
+struct LaneOffsets {
+  int dma[C::IPW];      // global byte offset of this lane's 16-byte chunk within a tile
+  int row[C::KS];       // LDS: b128 read of row l32, chunk 2 ks + g
+  int tr[C::DT][2];     // LDS: transposing read, rows 4g + (jr >> 2) (+8), columns of d tile
+  __device__ inline LaneOffsets(int w, int lane, int64_t tok_stride) {
+    const int l32 = lane & 31, g = lane >> 5, jr = lane & 15;
 #pragma unroll
-  for (int dt = 0; dt < C::DT; ++dt) dkt[dt] = dvt[dt] = f32x16{};
-
-  if (T > 0) {
-    bf16x8 kop[C::KS], vop[C::KS];
-    {
-      const int64_t off = base_bh + (int64_t)min(key, N - 1) * tok_stride + 8 * g;
-#pragma unroll
-      for (int ks = 0; ks < C::KS; ++ks) {
-        kop[ks] = *reinterpret_cast<const bf16x8*>(K + off + 16 * ks);
-        vop[ks] = *reinterpret_cast<const bf16x8*>(V + off + 16 * ks);
-      }
+    for (int u = 0; u < C::IPW; ++u) {
+      const int r = (w * C::IPW + u) * C::RPI + lane / C::CPR, p = lane % C::CPR;
+      const int c = (lds_off<C::CPR>(r, p) >> 4) & (C::CPR - 1);
+      dma[u] = r * (int)(tok_stride * 2) + 16 * c;
     }
-    u32x4 stg[C::LPT];
-    float stg_f = 0.f;
-    auto load_stage = [&](int t) __attribute__((always_inline)) {
-      const int i = rows_list[p0 + t / C::SUBS];
-      const int r0 = i * BLOCK + (t % C::SUBS) * C::ST;
 #pragma unroll
-      for (int u = 0; u < C::LPT; ++u) {
-        const int x = tid + C::NT * u;
-        const int isdo = x / (C::ST * C::CPR);
-        const int r = (x / C::CPR) % C::ST, c = x % C::CPR;
-        const int qr = min(r0 + r, N - 1);
-        stg[u] = *reinterpret_cast<const u32x4*>((isdo ? dO : Q) + base_bh + (int64_t)qr * tok_stride + 8 * c);
-      }
-      if (tid < 2 * C::ST) {
-        const int r = tid % C::ST, qr = r0 + r;
-        if (tid < C::ST)
-          stg_f = qr < N ? LSE[bh * N + qr] * kLog2e : INFINITY;   // rows past N: P = 0
-        else
-          stg_f = qr < N ? delta[bh * N + qr] : 0.f;
-      }
-    };
-    auto store_stage = [&](int s) __attribute__((always_inline)) {
-      char* st = smem + s * STAGEB;
-#pragma unroll
-      for (int u = 0; u < C::LPT; ++u) {
-        const int x = tid + C::NT * u;
-        const int isdo = x / (C::ST * C::CPR);
-        const int r = (x / C::CPR) % C::ST, c = x % C::CPR;
-        *reinterpret_cast<u32x4*>(st + isdo * C::TILEB + lds_off<C::CPR>(r, c)) = stg[u];
-      }
-      if (tid < 2 * C::ST) reinterpret_cast<float*>(st + 2 * C::TILEB)[tid] = stg_f;
-    };
-
-    const float c2 = scale * kLog2e;
-    const int jr = lane & 15;
+    for (int ks = 0; ks < C::KS; ++ks) row[ks] = lds_off<C::CPR>(l32, 2 * ks + g);
     const int dsub = 16 * ((lane >> 4) & 1) + 4 * (jr & 3);
-
-    load_stage(0);
-    store_stage(0);
-    __syncthreads();
-    for (int t = 0; t < T; ++t) {
-      const int cur = t & 1;
-      if (t + 1 < T) load_stage(t + 1);
-      const char* q_lds = smem + cur * STAGEB;
-      const char* do_lds = q_lds + C::TILEB;
-      const float* lse_lds = reinterpret_cast<const float*>(q_lds + 2 * C::TILEB);
-      const float* dl_lds = lse_lds + C::ST;
-
-      // S = Q K^T and dP = dO V^T, two 32-query tiles; lane column = key
-      f32x16 s[2] = {f32x16{}, f32x16{}}, dp[2] = {f32x16{}, f32x16{}};
-#pragma unroll
-      for (int ks = 0; ks < C::KS; ++ks)
-#pragma unroll
-        for (int qt = 0; qt < 2; ++qt) {
-          const int off = lds_off<C::CPR>(32 * qt + l32, 2 * ks + g);
-          s[qt] = mfma32(*reinterpret_cast<const bf16x8*>(q_lds + off), kop[ks], s[qt]);
-          dp[qt] = mfma32(*reinterpret_cast<const bf16x8*>(do_lds + off), vop[ks], dp[qt]);
-        }
-
-      bf16x8 pb[2][2], dsb[2][2];
-#pragma unroll
-      for (int qt = 0; qt < 2; ++qt)
-#pragma unroll
-        for (int a = 0; a < 4; ++a) {
-          const int r = 32 * qt + 8 * a + 4 * g;
-          const f32x4 l4 = *reinterpret_cast<const f32x4*>(lse_lds + r);
-          const f32x4 d4 = *reinterpret_cast<const f32x4*>(dl_lds + r);
-#pragma unroll
-          for (int e = 0; e < 4; ++e) {
-            const int idx = 4 * a + e;
-            const float p = fast_exp2(__builtin_fmaf(s[qt][idx], c2, -l4[e]));
-            const float ds = p * (dp[qt][idx] - d4[e]);
-            pb[qt][idx >> 3][idx & 7] = (__bf16)p;
-            dsb[qt][idx >> 3][idx & 7] = (__bf16)ds;
-          }
-        }
-
-      // dV^T += dO^T P and dK^T += Q^T dS (contraction over the 64 queries)
-#pragma unroll
-      for (int dt = 0; dt < C::DT; ++dt)
-#pragma unroll
-        for (int qt = 0; qt < 2; ++qt)
-#pragma unroll
-          for (int hh = 0; hh < 2; ++hh) {
-            const int r0 = 32 * qt + 16 * hh + 4 * g + (jr >> 2);
-            const int d = 32 * dt + dsub;
-            const int o_lo = lds_off<C::CPR>(r0, d >> 3) + 2 * (d & 7);
-            const int o_hi = lds_off<C::CPR>(r0 + 8, d >> 3) + 2 * (d & 7);
-            const s16x4 dlo = lds_read_tr16(do_lds + o_lo), dhi = lds_read_tr16(do_lds + o_hi);
-            const s16x4 qlo = lds_read_tr16(q_lds + o_lo), qhi = lds_read_tr16(q_lds + o_hi);
-            const s16x8 d8 = {dlo[0], dlo[1], dlo[2], dlo[3], dhi[0], dhi[1], dhi[2], dhi[3]};
-            const s16x8 q8 = {qlo[0], qlo[1], qlo[2], qlo[3], qhi[0], qhi[1], qhi[2], qhi[3]};
-            dvt[dt] = mfma32(__builtin_bit_cast(bf16x8, d8), pb[qt][hh], dvt[dt]);
-            dkt[dt] = mfma32(__builtin_bit_cast(bf16x8, q8), dsb[qt][hh], dkt[dt]);
-          }
-
-      if (t + 1 < T) store_stage(cur ^ 1);
-      __syncthreads();
-    }
-  }
-
-  if (key < N) {
-    const int64_t off = base_bh + (int64_t)key * tok_stride;
 #pragma unroll
     for (int dt = 0; dt < C::DT; ++dt)
 #pragma unroll
-      for (int a = 0; a < 4; ++a) {
-        bf16x4 k4, v4;
-#pragma unroll
-        for (int e = 0; e < 4; ++e) {
-          k4[e] = (__bf16)(dkt[dt][4 * a + e] * scale);
-          v4[e] = (__bf16)dvt[dt][4 * a + e];
-        }
-        *reinterpret_cast<bf16x4*>(dK + off + 32 * dt + 8 * a + 4 * g) = k4;
-        *reinterpret_cast<bf16x4*>(dV + off + 32 * dt + 8 * a + 4 * g) = v4;
+      for (int lh = 0; lh < 2; ++lh) {
+        const int d = 32 * dt + dsub;
+        tr[dt][lh] = lds_off<C::CPR>(4 * g + (jr >> 2) + 8 * lh, d >> 3) + 2 * (d & 7);
       }
   }
-}
+};
 
 // ---------------------------------------------------------------------------
 // dQ: query-stationary over the row lists
 // ---------------------------------------------------------------------------
 template <int D, int BLOCK>
-__global__ __launch_bounds__(64 * (BLOCK / 32), 1) void bwd_dq_kernel(
+__global__ __launch_bounds__(64 * (BLOCK / 32), (BLOCK == 128 || D == 64) ? 2 : 1) void bwd_dq_kernel(
     const __bf16* __restrict__ Q, const __bf16* __restrict__ K, const __bf16* __restrict__ V,
-    const __bf16* __restrict__ dO, const float* __restrict__ LSE, const float* __restrict__ delta,
-    __bf16* __restrict__ dQ, int B, int N, int H, int nblk, float scale,
-    const int32_t* __restrict__ rowptr, const int32_t* __restrict__ cols) {
-  using C = BwdCfg<D, BLOCK>;
-  constexpr int STAGEB = 2 * C::TILEB;   // K, V
-  __shared__ __attribute__((aligned(16))) char smem[2 * STAGEB];
+    const __bf16* __restrict__ dO, const float2* __restrict__ aux, __bf16* __restrict__ dQ, int B,
+    int N, int H, int nblk, float scale, const int32_t* __restrict__ rowptr,
+    const int32_t* __restrict__ cols) {
+  using C = BwdCfg<D, BLOCK, BLOCK / 32>;
+  __shared__ __attribute__((aligned(1024))) char k_lds0[C::TILEB];
+  __shared__ __attribute__((aligned(1024))) char k_lds1[C::TILEB];
+  __shared__ __attribute__((aligned(1024))) char v_lds0[C::TILEB];
+  __shared__ __attribute__((aligned(1024))) char v_lds1[C::TILEB];
 
-  const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int w = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int l32 = lane & 31, g = lane >> 5;
   const int64_t G = (int64_t)B * H * nblk;
   const int64_t lt = xcd_tile(blockIdx.x, G);
@@ -249,7 +130,6 @@ __global__ __launch_bounds__(64 * (BLOCK / 32), 1) void bwd_dq_kernel(
   const int h = (int)(bh % H), b = (int)(bh / H);
   const int64_t tok_stride = (int64_t)H * D;
   const int64_t base_bh = (int64_t)b * N * tok_stride + (int64_t)h * D;
-
   const int q = i * BLOCK + 32 * w + l32;
   const int p0 = rowptr[lt], p1 = rowptr[lt + 1];
   const int T = (p1 - p0) * C::SUBS;
@@ -268,86 +148,99 @@ __global__ __launch_bounds__(64 * (BLOCK / 32), 1) void bwd_dq_kernel(
         doop[ks] = *reinterpret_cast<const bf16x8*>(dO + off + 16 * ks);
       }
     }
-    const float lse2 = q < N ? LSE[bh * N + q] * kLog2e : INFINITY;
-    const float dl = q < N ? delta[bh * N + q] : 0.f;
+    const float2 a2 = aux[bh * N + min(q, N - 1)];
+    const float lse2 = a2.x, dl = a2.y;
+    const LaneOffsets<C> lo(w, lane, tok_stride);
 
-    u32x4 stg[C::LPT];
-    auto load_stage = [&](int t) __attribute__((always_inline)) {
+    auto load_tile = [&](const __bf16* X, int t, char* dst) __attribute__((always_inline)) {
       const int j = cols[p0 + t / C::SUBS];
-      const int k0 = j * BLOCK + (t % C::SUBS) * C::ST;
+      const int key0 = j * BLOCK + (t % C::SUBS) * C::ST;
+      const int nrec = key0 < N ? (N - key0 - 1) * (int)(tok_stride * 2) + 2 * D : 0;
+      const __amdgpu_buffer_rsrc_t rs = buffer_rsrc(X + base_bh + (int64_t)key0 * tok_stride, nrec);
 #pragma unroll
-      for (int u = 0; u < C::LPT; ++u) {
-        const int x = tid + C::NT * u;
-        const int isv = x / (C::ST * C::CPR);
-        const int r = (x / C::CPR) % C::ST, c = x % C::CPR;
-        const int kr = min(k0 + r, N - 1);
-        stg[u] = *reinterpret_cast<const u32x4*>((isv ? V : K) + base_bh + (int64_t)kr * tok_stride + 8 * c);
-      }
+      for (int u = 0; u < C::IPW; ++u) buffer_load_lds16(rs, dst + (w * C::IPW + u) * 1024, lo.dma[u]);
     };
-    auto store_stage = [&](int s) __attribute__((always_inline)) {
-      char* st = smem + s * STAGEB;
-#pragma unroll
-      for (int u = 0; u < C::LPT; ++u) {
-        const int x = tid + C::NT * u;
-        const int isv = x / (C::ST * C::CPR);
-        const int r = (x / C::CPR) % C::ST, c = x % C::CPR;
-        *reinterpret_cast<u32x4*>(st + isv * C::TILEB + lds_off<C::CPR>(r, c)) = stg[u];
-      }
-    };
-
     const float c2 = scale * kLog2e;
-    const int jr = lane & 15;
-    const int dsub = 16 * ((lane >> 4) & 1) + 4 * (jr & 3);
 
-    load_stage(0);
-    store_stage(0);
-    __syncthreads();
-    for (int t = 0; t < T; ++t) {
-      const int cur = t & 1;
-      if (t + 1 < T) load_stage(t + 1);
-      const char* k_lds = smem + cur * STAGEB;
-      const char* v_lds = k_lds + C::TILEB;
-
+    auto step = [&](int t, const char* kt_lds, const char* vt_lds, auto masked)
+        __attribute__((always_inline)) {
       f32x16 s[2] = {f32x16{}, f32x16{}}, dp[2] = {f32x16{}, f32x16{}};
 #pragma unroll
       for (int ks = 0; ks < C::KS; ++ks)
 #pragma unroll
         for (int kt = 0; kt < 2; ++kt) {
-          const int off = lds_off<C::CPR>(32 * kt + l32, 2 * ks + g);
-          s[kt] = mfma32(*reinterpret_cast<const bf16x8*>(k_lds + off), qop[ks], s[kt]);
-          dp[kt] = mfma32(*reinterpret_cast<const bf16x8*>(v_lds + off), doop[ks], dp[kt]);
+          const int off = lo.row[ks] + kt * 32 * C::ROWB;
+          s[kt] = mfma32(*reinterpret_cast<const bf16x8*>(kt_lds + off), qop[ks], s[kt]);
+          dp[kt] = mfma32(*reinterpret_cast<const bf16x8*>(vt_lds + off), doop[ks], dp[kt]);
         }
-
-      const int j = cols[p0 + t / C::SUBS];
-      const int k0 = j * BLOCK + (t % C::SUBS) * C::ST;
-      const bool tail = k0 + C::ST > N;
+      int lim = C::ST;
+      if constexpr (decltype(masked)::value) {   // keys past N in a short last block
+        const int j = cols[p0 + t / C::SUBS];
+        lim = N - (j * BLOCK + (t % C::SUBS) * C::ST);
+      }
       bf16x8 dsb[2][2];
+      __builtin_amdgcn_sched_barrier(0);   // keep the dQ operand reads below (register pressure)
 #pragma unroll
       for (int kt = 0; kt < 2; ++kt)
 #pragma unroll
         for (int e = 0; e < 16; ++e) {
           float p = fast_exp2(__builtin_fmaf(s[kt][e], c2, -lse2));
-          if (tail && k0 + 32 * kt + 8 * (e >> 2) + 4 * g + (e & 3) >= N) p = 0.f;
+          if constexpr (decltype(masked)::value)
+            p = 32 * kt + 8 * (e >> 2) + 4 * g + (e & 3) >= lim ? 0.f : p;
           dsb[kt][e >> 3][e & 7] = (__bf16)(p * (dp[kt][e] - dl));
         }
-
-      // dQ^T += K^T dS^T (contraction over the 64 keys)
+      __builtin_amdgcn_sched_barrier(0);
+      // dQ^T += K^T dS^T: K^T tile kt, half hh covers keys 32kt + 16hh + {4g+0..3, 8+4g+0..3}
 #pragma unroll
       for (int dt = 0; dt < C::DT; ++dt)
 #pragma unroll
         for (int kt = 0; kt < 2; ++kt)
 #pragma unroll
           for (int hh = 0; hh < 2; ++hh) {
-            const int r0 = 32 * kt + 16 * hh + 4 * g + (jr >> 2);
-            const int d = 32 * dt + dsub;
-            const s16x4 lo = lds_read_tr16(k_lds + lds_off<C::CPR>(r0, d >> 3) + 2 * (d & 7));
-            const s16x4 hi = lds_read_tr16(k_lds + lds_off<C::CPR>(r0 + 8, d >> 3) + 2 * (d & 7));
-            const s16x8 k8 = {lo[0], lo[1], lo[2], lo[3], hi[0], hi[1], hi[2], hi[3]};
+            const char* kb = kt_lds + (32 * kt + 16 * hh) * C::ROWB;
+            const s16x4 l4 = lds_read_tr16(kb + lo.tr[dt][0]);
+            const s16x4 h4 = lds_read_tr16(kb + lo.tr[dt][1]);
+            const s16x8 k8 = {l4[0], l4[1], l4[2], l4[3], h4[0], h4[1], h4[2], h4[3]};
             dqt[dt] = mfma32(__builtin_bit_cast(bf16x8, k8), dsb[kt][hh], dqt[dt]);
           }
-
-      if (t + 1 < T) store_stage(cur ^ 1);
+    };
+    auto iter = [&](int t, auto par, auto masked) __attribute__((always_inline)) {
+      constexpr int P = decltype(par)::value;
+      if (t + 1 < T) {
+        load_tile(K, t + 1, P ? k_lds0 : k_lds1);
+        load_tile(V, t + 1, P ? v_lds0 : v_lds1);
+      }
+      step(t, P ? k_lds1 : k_lds0, P ? v_lds1 : v_lds0, masked);
+      __builtin_amdgcn_s_waitcnt(0);
       __syncthreads();
+    };
+
+    load_tile(K, 0, k_lds0);
+    load_tile(V, 0, v_lds0);
+    __builtin_amdgcn_s_waitcnt(0);
+    __syncthreads();
+    const bool tail = (N % BLOCK != 0) && cols[p1 - 1] == nblk - 1;
+    const int Tm = tail ? T - C::SUBS : T;
+    using I0 = std::integral_constant<int, 0>;
+    using I1 = std::integral_constant<int, 1>;
+    using F = std::false_type;
+    using Tt = std::true_type;
+    int t = 0;
+    for (; t + 1 < Tm; t += 2) {
+      iter(t, I0{}, F{});
+      iter(t + 1, I1{}, F{});
+    }
+    if (t < Tm) {
+      iter(t, I0{}, F{});
+      for (++t; t < T; t += 2) {
+        iter(t, I1{}, Tt{});
+        if (t + 1 < T) iter(t + 1, I0{}, Tt{});
+      }
+    } else {
+      for (; t < T; t += 2) {
+        iter(t, I0{}, Tt{});
+        if (t + 1 < T) iter(t + 1, I1{}, Tt{});
+      }
     }
   }
 
@@ -356,31 +249,223 @@ __global__ __launch_bounds__(64 * (BLOCK / 32), 1) void bwd_dq_kernel(
 #pragma unroll
     for (int dt = 0; dt < C::DT; ++dt)
 #pragma unroll
-      for (int a = 0; a < 4; ++a) {
+      for (int e4 = 0; e4 < 4; ++e4) {
         bf16x4 v4;
 #pragma unroll
-        for (int e = 0; e < 4; ++e) v4[e] = (__bf16)(dqt[dt][4 * a + e] * scale);
-        *reinterpret_cast<bf16x4*>(dQ + off + 32 * dt + 8 * a + 4 * g) = v4;
+        for (int e = 0; e < 4; ++e) v4[e] = (__bf16)(dqt[dt][4 * e4 + e] * scale);
+        *reinterpret_cast<bf16x4*>(dQ + off + 32 * dt + 8 * e4 + 4 * g) = v4;
       }
   }
+}
+
+// ---------------------------------------------------------------------------
+// dK, dV: key-stationary over the column lists, two waves per 32 keys
+// ---------------------------------------------------------------------------
+template <int D, int BLOCK>
+__global__ __launch_bounds__(128 * (BLOCK / 32), 1) void bwd_dkdv_kernel(
+    const __bf16* __restrict__ Q, const __bf16* __restrict__ K, const __bf16* __restrict__ V,
+    const __bf16* __restrict__ dO, const float2* __restrict__ aux, __bf16* __restrict__ dK,
+    __bf16* __restrict__ dV, int B, int N, int H, int nblk, float scale,
+    const int32_t* __restrict__ colptr, const int32_t* __restrict__ rows_list) {
+  constexpr int NK = BLOCK / 32;        // key groups (waves per query half)
+  using C = BwdCfg<D, BLOCK, 2 * NK>;
+  constexpr int AUXB = 1024;            // 64 rows x 8 bytes, padded to one load
+  __shared__ __attribute__((aligned(1024))) char q_lds0[C::TILEB];
+  __shared__ __attribute__((aligned(1024))) char q_lds1[C::TILEB];
+  __shared__ __attribute__((aligned(1024))) char o_lds0[C::TILEB];
+  __shared__ __attribute__((aligned(1024))) char o_lds1[C::TILEB];
+  __shared__ __attribute__((aligned(1024))) char a_lds0[AUXB];
+  __shared__ __attribute__((aligned(1024))) char a_lds1[AUXB];
+  // V rows of this key block (the B operand of dP = dO V^T), loaded once
+  __shared__ __attribute__((aligned(1024))) char vblk_lds[BLOCK * C::ROWB];
+
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int w = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int kw = w % NK, qh = w / NK;   // 32-key group, query half of each tile
+  const int l32 = lane & 31, g = lane >> 5;
+  const int64_t G = (int64_t)B * H * nblk;
+  const int64_t lt = xcd_tile(blockIdx.x, G);
+  const int j = (int)(lt % nblk);
+  const int64_t bh = lt / nblk;
+  const int h = (int)(bh % H), b = (int)(bh / H);
+  const int64_t tok_stride = (int64_t)H * D;
+  const int64_t base_bh = (int64_t)b * N * tok_stride + (int64_t)h * D;
+  const int key = j * BLOCK + 32 * kw + l32;
+  const int p0 = colptr[lt], p1 = colptr[lt + 1];
+  const int T = (p1 - p0) * C::SUBS;
+
+  f32x16 dkt[C::DT], dvt[C::DT];
+#pragma unroll
+  for (int dt = 0; dt < C::DT; ++dt) dkt[dt] = dvt[dt] = f32x16{};
+
+  if (T > 0) {
+    bf16x8 kop[C::KS];
+    {
+      const int64_t off = base_bh + (int64_t)min(key, N - 1) * tok_stride + 8 * g;
+#pragma unroll
+      for (int ks = 0; ks < C::KS; ++ks) kop[ks] = *reinterpret_cast<const bf16x8*>(K + off + 16 * ks);
+    }
+    const LaneOffsets<C> lo(w, lane, tok_stride);
+    {   // V block: BLOCK rows in the swizzled row layout (rows past N read zeros)
+      const int k0 = j * BLOCK;
+      const int nrec = (N - k0 - 1) * (int)(tok_stride * 2) + 2 * D;
+      const __amdgpu_buffer_rsrc_t rv = buffer_rsrc(V + base_bh + (int64_t)k0 * tok_stride, nrec);
+#pragma unroll
+      for (int half = 0; half < C::SUBS; ++half)
+#pragma unroll
+        for (int u = 0; u < C::IPW; ++u)
+          buffer_load_lds16(rv, vblk_lds + half * C::TILEB + (w * C::IPW + u) * 1024,
+                            lo.dma[u] + half * C::ST * (int)(tok_stride * 2));
+    }
+    const char* const vrow = vblk_lds + 32 * kw * C::ROWB;   // this wave's 32 keys
+
+    // Tile t: 64 query rows of Q and dO, and their {LSE log2 e, delta}.
+    auto load_tile = [&](int t, char* qd, char* od, char* ad) __attribute__((always_inline)) {
+      const int i = rows_list[p0 + t / C::SUBS];
+      const int r0 = i * BLOCK + (t % C::SUBS) * C::ST;
+      const int nrec = r0 < N ? (N - r0 - 1) * (int)(tok_stride * 2) + 2 * D : 0;
+      const __amdgpu_buffer_rsrc_t rq = buffer_rsrc(Q + base_bh + (int64_t)r0 * tok_stride, nrec);
+      const __amdgpu_buffer_rsrc_t ro = buffer_rsrc(dO + base_bh + (int64_t)r0 * tok_stride, nrec);
+#pragma unroll
+      for (int u = 0; u < C::IPW; ++u) {
+        buffer_load_lds16(rq, qd + (w * C::IPW + u) * 1024, lo.dma[u]);
+        buffer_load_lds16(ro, od + (w * C::IPW + u) * 1024, lo.dma[u]);
+      }
+      if (w == 0) {   // rows past N (and lanes past the 64 rows) read zeros
+        const __amdgpu_buffer_rsrc_t ra =
+            buffer_rsrc(aux + bh * N + r0, r0 < N ? min(N - r0, C::ST) * 8 : 0);
+        buffer_load_lds16(ra, ad, 16 * lane);
+      }
+    };
+    const float c2 = scale * kLog2e;
+
+    auto step = [&](const char* qt_lds, const char* ot_lds, const char* at_lds)
+        __attribute__((always_inline)) {
+      // S = Q K^T and dP = dO V^T for this wave's 32 query rows (32 qh ..)
+      f32x16 s = f32x16{}, dp = f32x16{};
+#pragma unroll
+      for (int ks = 0; ks < C::KS; ++ks) {
+        const int off = lo.row[ks] + 32 * qh * C::ROWB;
+        s = mfma32(*reinterpret_cast<const bf16x8*>(qt_lds + off), kop[ks], s);
+        const bf16x8 vop = *reinterpret_cast<const bf16x8*>(vrow + lo.row[ks]);
+        dp = mfma32(*reinterpret_cast<const bf16x8*>(ot_lds + off), vop, dp);
+      }
+      // rows 32 qh + 8 a + 4 g + (0..3): P and dS, as the B operands of the
+      // second products (half hh: rows 16 hh + {4g+0..3, 8+4g+0..3})
+      bf16x8 pb[2], dsb[2];
+#pragma unroll
+      for (int a = 0; a < 4; ++a) {
+        const float* ap = reinterpret_cast<const float*>(at_lds) + 2 * (32 * qh + 8 * a + 4 * g);
+        const f32x4 x0 = *reinterpret_cast<const f32x4*>(ap);       // rows +0, +1
+        const f32x4 x1 = *reinterpret_cast<const f32x4*>(ap + 4);   // rows +2, +3
+        const float ls[4] = {x0[0], x0[2], x1[0], x1[2]};
+        const float dl[4] = {x0[1], x0[3], x1[1], x1[3]};
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          const int idx = 4 * a + e;
+          const float p = fast_exp2(__builtin_fmaf(s[idx], c2, -ls[e]));
+          pb[idx >> 3][idx & 7] = (__bf16)p;
+          dsb[idx >> 3][idx & 7] = (__bf16)(p * (dp[idx] - dl[e]));
+        }
+      }
+      // dV^T += dO^T P and dK^T += Q^T dS over this wave's 32 query rows
+#pragma unroll
+      for (int dt = 0; dt < C::DT; ++dt)
+#pragma unroll
+        for (int hh = 0; hh < 2; ++hh) {
+          const int rb = (32 * qh + 16 * hh) * C::ROWB;
+          const s16x4 o_lo = lds_read_tr16(ot_lds + rb + lo.tr[dt][0]);
+          const s16x4 o_hi = lds_read_tr16(ot_lds + rb + lo.tr[dt][1]);
+          const s16x4 q_lo = lds_read_tr16(qt_lds + rb + lo.tr[dt][0]);
+          const s16x4 q_hi = lds_read_tr16(qt_lds + rb + lo.tr[dt][1]);
+          const s16x8 o8 = {o_lo[0], o_lo[1], o_lo[2], o_lo[3], o_hi[0], o_hi[1], o_hi[2], o_hi[3]};
+          const s16x8 q8 = {q_lo[0], q_lo[1], q_lo[2], q_lo[3], q_hi[0], q_hi[1], q_hi[2], q_hi[3]};
+          dvt[dt] = mfma32(__builtin_bit_cast(bf16x8, o8), pb[hh], dvt[dt]);
+          dkt[dt] = mfma32(__builtin_bit_cast(bf16x8, q8), dsb[hh], dkt[dt]);
+        }
+    };
+    auto iter = [&](int t, auto par) __attribute__((always_inline)) {
+      constexpr int P = decltype(par)::value;
+      if (t + 1 < T) load_tile(t + 1, P ? q_lds0 : q_lds1, P ? o_lds0 : o_lds1, P ? a_lds0 : a_lds1);
+      step(P ? q_lds1 : q_lds0, P ? o_lds1 : o_lds0, P ? a_lds1 : a_lds0);
+      __builtin_amdgcn_s_waitcnt(0);
+      __syncthreads();
+    };
+
+    load_tile(0, q_lds0, o_lds0, a_lds0);
+    __builtin_amdgcn_s_waitcnt(0);
+    __syncthreads();
+    using I0 = std::integral_constant<int, 0>;
+    using I1 = std::integral_constant<int, 1>;
+    int t = 0;
+    for (; t + 1 < T; t += 2) {
+      iter(t, I0{});
+      iter(t + 1, I1{});
+    }
+    if (t < T) iter(t, I0{});
+  }
+
+  // The two query halves meet: the second half's partial sums go through LDS
+  // (one 16 KB region per key group), the first half adds them and stores.
+  char* const region = kw == 0 ? q_lds0 : kw == 1 ? q_lds1 : kw == 2 ? o_lds0 : o_lds1;
+  f32x4* const part = reinterpret_cast<f32x4*>(region) + lane;
+  auto store_out = [&](__bf16* X, const f32x16 (&acc)[C::DT], float mul) __attribute__((always_inline)) {
+    if (key >= N) return;
+    const int64_t off = base_bh + (int64_t)key * tok_stride;
+#pragma unroll
+    for (int dt = 0; dt < C::DT; ++dt)
+#pragma unroll
+      for (int e4 = 0; e4 < 4; ++e4) {
+        bf16x4 v4;
+#pragma unroll
+        for (int e = 0; e < 4; ++e) v4[e] = (__bf16)(acc[dt][4 * e4 + e] * mul);
+        *reinterpret_cast<bf16x4*>(X + off + 32 * dt + 8 * e4 + 4 * g) = v4;
+      }
+  };
+  auto merge = [&](f32x16 (&acc)[C::DT]) __attribute__((always_inline)) {
+    if (qh == 1) {
+#pragma unroll
+      for (int dt = 0; dt < C::DT; ++dt)
+#pragma unroll
+        for (int e4 = 0; e4 < 4; ++e4)
+          part[(4 * dt + e4) * 64] = f32x4{acc[dt][4 * e4], acc[dt][4 * e4 + 1], acc[dt][4 * e4 + 2],
+                                           acc[dt][4 * e4 + 3]};
+    }
+    __syncthreads();
+    if (qh == 0) {
+#pragma unroll
+      for (int dt = 0; dt < C::DT; ++dt)
+#pragma unroll
+        for (int e4 = 0; e4 < 4; ++e4) {
+          const f32x4 x = part[(4 * dt + e4) * 64];
+#pragma unroll
+          for (int e = 0; e < 4; ++e) acc[dt][4 * e4 + e] += x[e];
+        }
+    }
+    __syncthreads();
+  };
+  merge(dkt);
+  if (qh == 0) store_out(dK, dkt, scale);
+  merge(dvt);
+  if (qh == 0) store_out(dV, dvt, 1.f);
 }
 
 template <int D, int BLOCK>
 hipError_t launch_bwd_t(const void* q, const void* k, const void* v, const void* o,
                         const void* dout, const float* lse, void* dq, void* dk, void* dv,
                         const AttnShape& sh, const int32_t* rowptr, const int32_t* cols,
-                        const int32_t* colptr, const int32_t* rows, float* delta, hipStream_t s) {
+                        const int32_t* colptr, const int32_t* rows, float* ws, hipStream_t s) {
   auto bf = [](const void* p) { return static_cast<const __bf16*>(p); };
+  float2* aux = reinterpret_cast<float2*>(ws);
   const int64_t rows_total = (int64_t)sh.B * sh.N * sh.H * (D / 8);
-  hipLaunchKernelGGL((bwd_delta_kernel<D>), dim3((unsigned)((rows_total + 255) / 256)), dim3(256), 0,
-                     s, bf(o), bf(dout), delta, sh.B, sh.N, sh.H);
+  hipLaunchKernelGGL((bwd_prep_kernel<D>), dim3((unsigned)((rows_total + 255) / 256)), dim3(256), 0,
+                     s, bf(o), bf(dout), lse, aux, sh.B, sh.N, sh.H);
   const int64_t G = (int64_t)sh.B * sh.H * sh.nblk;
-  constexpr int NT = BwdCfg<D, BLOCK>::NT;
-  hipLaunchKernelGGL((bwd_dkdv_kernel<D, BLOCK>), dim3((unsigned)G), dim3(NT), 0, s, bf(q), bf(k),
-                     bf(v), bf(dout), lse, delta, static_cast<__bf16*>(dk),
+  hipLaunchKernelGGL((bwd_dkdv_kernel<D, BLOCK>), dim3((unsigned)G), dim3(128 * (BLOCK / 32)), 0, s,
+                     bf(q), bf(k), bf(v), bf(dout), aux, static_cast<__bf16*>(dk),
                      static_cast<__bf16*>(dv), sh.B, sh.N, sh.H, sh.nblk, sh.scale, colptr, rows);
-  hipLaunchKernelGGL((bwd_dq_kernel<D, BLOCK>), dim3((unsigned)G), dim3(NT), 0, s, bf(q), bf(k),
-                     bf(v), bf(dout), lse, delta, static_cast<__bf16*>(dq), sh.B, sh.N, sh.H,
+  hipLaunchKernelGGL((bwd_dq_kernel<D, BLOCK>), dim3((unsigned)G), dim3(64 * (BLOCK / 32)), 0, s,
+                     bf(q), bf(k), bf(v), bf(dout), aux, static_cast<__bf16*>(dq), sh.B, sh.N, sh.H,
                      sh.nblk, sh.scale, rowptr, cols);
   return hipGetLastError();
 }

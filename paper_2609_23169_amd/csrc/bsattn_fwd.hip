@@ -36,14 +36,6 @@ namespace {
 constexpr float kLog2e = 1.4426950408889634f;
 constexpr float kLn2 = 0.6931471805599453f;
 constexpr float kRescaleSlack = 8.0f;   // log2 units: p = 2^(s - m) stays <= 256
-constexpr int kRsrcWord3 = 0x00020000;  // raw buffer, 32-bit data format
-
-// One 16-byte-per-lane buffer load straight into LDS: lane L writes at
-// lds + 16 L (lds must be wave-uniform).
-__device__ inline void buffer_load_lds16(__amdgpu_buffer_rsrc_t rs, char* lds, int voffset) {
-  __builtin_amdgcn_raw_ptr_buffer_load_lds(rs, (__attribute__((address_space(3))) void*)lds, 16,
-                                           voffset, 0, 0, 0);
-}
 
 template <int D, int BLOCK>
 struct FwdCfg {
@@ -130,8 +122,7 @@ __global__ __launch_bounds__(64 * (BLOCK / 32), (BLOCK == 128 || D == 64) ? 2 : 
     // a sub-tile wholly past N (second half of a short last block) gets an
     // empty range: every load reads zeros and nothing past the tensor is touched
     const int nrec = key0 < N ? (N - key0 - 1) * (int)(tok_stride * 2) + 2 * D : 0;
-    const __amdgpu_buffer_rsrc_t rs = __builtin_amdgcn_make_buffer_rsrc(
-        const_cast<__bf16*>(tile), (short)0, nrec, kRsrcWord3);
+    const __amdgpu_buffer_rsrc_t rs = buffer_rsrc(tile, nrec);
 #pragma unroll
     for (int u = 0; u < C::IPW; ++u)
       buffer_load_lds16(rs, dst + (w * C::IPW + u) * 1024, dma_off[u]);

@@ -35,7 +35,7 @@ def test_workspace_sizes():
     assert ut.ut_drop_background_workspace_size(212992) == 52 * 4
     assert ut.ut_drop_background_workspace_size(1) == 4
     assert ut.ut_drop_background_workspace_size(0) == 0
-    assert ut.ut_bsattn_bwd_workspace_size(1, 77586, 24) == 77586 * 24 * 4
+    assert ut.ut_bsattn_bwd_workspace_size(1, 77586, 24) == 77586 * 24 * 8
 
 
 def _fwd(**kw):
@@ -66,10 +66,10 @@ def test_bwd_rejects_missing_workspace():
     args = [FAKE] * 9 + [1, 100, 2, 128, 128] + [FAKE] * 4 + [0.1]
     st = lib.ut_bsattn_bwd(*args, None, 0, None)
     assert st == ut.UT_ERR_WORKSPACE and "workspace" in ut.last_error()
-    st = lib.ut_bsattn_bwd(*args, FAKE, 100 * 2 * 4 - 4, None)
+    st = lib.ut_bsattn_bwd(*args, FAKE, 100 * 2 * 8 - 4, None)
     assert st == ut.UT_ERR_WORKSPACE
     args[2] = None
-    assert lib.ut_bsattn_bwd(*args, FAKE, 800, None) == ut.UT_ERR_INVALID_ARG
+    assert lib.ut_bsattn_bwd(*args, FAKE, 1600, None) == ut.UT_ERR_INVALID_ARG
 
 
 def test_drop_background_rejects_bad_arguments():
