@@ -29,6 +29,7 @@ sys.path.insert(0, ROOT)
 
 PEAK_BF16_TFLOPS = 2516.6     # MI355X dense bf16 MFMA (256 CU x 2.4 GHz x 4096 FLOP/clk)
 PEAK_HBM_GBS = 8000.0
+CAL_COPY_BYTES = 1 << 28      # calibration copy: 256 MiB read + 256 MiB written
 
 
 def parse():
@@ -143,6 +144,13 @@ def main():
         if hidden is not None:
             check(ut.ut_scatter_foreground(packed, kept, n, full_out), "scatter")
         rec(5)
+
+    # Untimed plain device-to-device copy of known size: under rocprofv3 --pmc
+    # its FETCH_SIZE / WRITE_SIZE calibrate the counters to bytes.
+    cal_src = torch.empty(CAL_COPY_BYTES, dtype=torch.uint8, device=dev)
+    cal_dst = torch.empty_like(cal_src)
+    cal_dst.copy_(cal_src)
+    del cal_src, cal_dst
 
     for _ in range(args.warmup):
         step()

@@ -68,13 +68,4 @@ __device__ inline void buffer_load_lds16(__amdgpu_buffer_rsrc_t rs, char* lds, i
                                            voffset, 0, 0, 0);
 }
 
-// Workgroups are dispatched round-robin over the 8 XCDs (workgroup w runs on
-// XCD w % 8). Renumber so each XCD receives one contiguous range of logical
-// tiles: neighbouring query blocks of one head then share that XCD's L2.
-__device__ inline int64_t xcd_tile(int64_t w, int64_t G) {
-  const int64_t xcd = w % 8, slot = w / 8;
-  const int64_t per = G / 8, rem = G % 8;
-  return xcd * per + (xcd < rem ? xcd : rem) + slot;
-}
-
 }  // namespace ut

@@ -123,8 +123,7 @@ __global__ __launch_bounds__(64 * (BLOCK / 32), (BLOCK == 128 || D == 64) ? 2 : 
   const int tid = threadIdx.x, lane = tid & 63;
   const int w = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int l32 = lane & 31, g = lane >> 5;
-  const int64_t G = (int64_t)B * H * nblk;
-  const int64_t lt = xcd_tile(blockIdx.x, G);
+  const int64_t lt = blockIdx.x;   // tile order: see the launcher
   const int i = (int)(lt % nblk);
   const int64_t bh = lt / nblk;
   const int h = (int)(bh % H), b = (int)(bh / H);
@@ -283,8 +282,7 @@ __global__ __launch_bounds__(128 * (BLOCK / 32), 1) void bwd_dkdv_kernel(
   const int w = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int kw = w % NK, qh = w / NK;   // 32-key group, query half of each tile
   const int l32 = lane & 31, g = lane >> 5;
-  const int64_t G = (int64_t)B * H * nblk;
-  const int64_t lt = xcd_tile(blockIdx.x, G);
+  const int64_t lt = blockIdx.x;   // tile order: see the launcher
   const int j = (int)(lt % nblk);
   const int64_t bh = lt / nblk;
   const int h = (int)(bh % H), b = (int)(bh / H);
@@ -460,11 +458,15 @@ hipError_t launch_bwd_t(const void* q, const void* k, const void* v, const void*
   const int64_t rows_total = (int64_t)sh.B * sh.N * sh.H * (D / 8);
   hipLaunchKernelGGL((bwd_prep_kernel<D>), dim3((unsigned)((rows_total + 255) / 256)), dim3(256), 0,
                      s, bf(o), bf(dout), lse, aux, sh.B, sh.N, sh.H);
-  const int64_t G = (int64_t)sh.B * sh.H * sh.nblk;
-  hipLaunchKernelGGL((bwd_dkdv_kernel<D, BLOCK>), dim3((unsigned)G), dim3(128 * (BLOCK / 32)), 0, s,
+  // One workgroup per (b, h, block) in plain order. Workgroups go round-robin
+  // to the 8 XCDs, so all XCDs work on the same few heads at once (their K and
+  // V stay in the shared last-level cache) and a run of heavy blocks is spread
+  // over every XCD.
+  const dim3 grid((unsigned)((int64_t)sh.B * sh.H * sh.nblk));
+  hipLaunchKernelGGL((bwd_dkdv_kernel<D, BLOCK>), grid, dim3(128 * (BLOCK / 32)), 0, s,
                      bf(q), bf(k), bf(v), bf(dout), aux, static_cast<__bf16*>(dk),
                      static_cast<__bf16*>(dv), sh.B, sh.N, sh.H, sh.nblk, sh.scale, colptr, rows);
-  hipLaunchKernelGGL((bwd_dq_kernel<D, BLOCK>), dim3((unsigned)G), dim3(64 * (BLOCK / 32)), 0, s,
+  hipLaunchKernelGGL((bwd_dq_kernel<D, BLOCK>), grid, dim3(64 * (BLOCK / 32)), 0, s,
                      bf(q), bf(k), bf(v), bf(dout), aux, static_cast<__bf16*>(dq), sh.B, sh.N, sh.H,
                      sh.nblk, sh.scale, rowptr, cols);
   return hipGetLastError();

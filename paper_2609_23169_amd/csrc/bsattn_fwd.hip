@@ -69,8 +69,7 @@ __global__ __launch_bounds__(64 * (BLOCK / 32), (BLOCK == 128 || D == 64) ? 2 : 
   const int tid = threadIdx.x, lane = tid & 63;
   const int w = __builtin_amdgcn_readfirstlane(tid >> 6);   // wave index, uniform
   const int l32 = lane & 31, g = lane >> 5;
-  const int64_t G = (int64_t)B * H * nblk;
-  const int64_t lt = xcd_tile(blockIdx.x, G);
+  const int64_t lt = blockIdx.x;   // tile order: see the launcher
   const int i = (int)(lt % nblk);
   const int64_t bh = lt / nblk;
   const int h = (int)(bh % H), b = (int)(bh / H);
@@ -283,8 +282,12 @@ template <int D, int BLOCK>
 hipError_t launch_fwd_t(const void* q, const void* k, const void* v, void* o, float* lse,
                         const AttnShape& sh, const int32_t* rowptr, const int32_t* cols,
                         hipStream_t s) {
-  const int64_t G = (int64_t)sh.B * sh.H * sh.nblk;
-  hipLaunchKernelGGL((bsattn_fwd_kernel<D, BLOCK>), dim3((unsigned)G), dim3(FwdCfg<D, BLOCK>::NT), 0,
+  // One workgroup per (b, h, block) in plain order. Workgroups go round-robin
+  // to the 8 XCDs, so all XCDs work on the same few heads at once (their K and
+  // V stay in the shared last-level cache) and a run of heavy blocks is spread
+  // over every XCD.
+  const dim3 grid((unsigned)((int64_t)sh.B * sh.H * sh.nblk));
+  hipLaunchKernelGGL((bsattn_fwd_kernel<D, BLOCK>), grid, dim3(FwdCfg<D, BLOCK>::NT), 0,
                      s, static_cast<const __bf16*>(q), static_cast<const __bf16*>(k),
                      static_cast<const __bf16*>(v), static_cast<__bf16*>(o), lse, sh.B, sh.N, sh.H,
                      sh.nblk, sh.scale, rowptr, cols);
