@@ -18,6 +18,9 @@ Paper sections (arXiv 2609.23169, "UltraTex"):
   * Block-Sparse Attention: Sec. 3.3, Eq. 5 (dense softmax attention with
     scale 1/sqrt(d)), the b_q / b_kv block partition, Eq. 7 (binary block mask
     M_c) and Eq. 8 (each query block attends only to its selected key blocks).
+  * Top-K block selection: Sec. 3.3, Eq. 6 (compressed scores from
+    mean-pooled query and key blocks) and Eq. 7 (row-wise Top-K over the key
+    blocks gives the block mask).
   * The backward pass: the paper trains its third stage with block-sparse
     attention but prints no gradient formula; the oracle differentiates Eq. 8
     with the mask held constant (the standard softmax-attention gradient
@@ -30,6 +33,7 @@ import numpy as np
 __all__ = [
     "compact", "gather", "scatter", "block_index",
     "bsattn_fwd", "bsattn_bwd",
+    "block_pool", "topk_block_mask",
 ]
 
 
@@ -214,3 +218,49 @@ def bsattn_bwd(q, k, v, dout, block_mask, block: int, scale: float,
                 dV[b, keys, h, :] += P.T @ dOi
     return dQ, dK, dV
 
+
+
+# ---------------------------------------------------------------------------
+# Top-K block selection (Sec. 3.3, Eq. 6 and Eq. 7)
+# ---------------------------------------------------------------------------
+
+def block_pool(x, block: int) -> np.ndarray:
+    """pool(.) of Eq. 6: the mean of each block's token rows, per head.
+
+    x [B, N, H, D] -> [B, H, ceil(N / block), D] float64. A short last block is
+    averaged over its real tokens (the reading taken for a ragged tail).
+    """
+    X = _f64(x)
+    B, N, H, D = X.shape
+    nb = -(-N // block)
+    out = np.zeros((B, H, nb, D))
+    for b in range(B):
+        for h in range(H):
+            for j in range(nb):
+                rows = _block_tokens(j, block, N)
+                out[b, h, j] = X[b, rows, h, :].sum(axis=0) / rows.size
+    return out
+
+
+def topk_block_mask(q, k, block: int, k_keep: int):
+    """Eq. 6-7: per (b, h), S_c = pool(Q) pool(K)^T and M_c[i, j] = 1 for the
+    k_keep largest entries of row i of S_c.
+
+    Readings: the paper keeps floor(rho N_k) blocks and the caller passes that
+    count as k_keep (k_keep >= N_k keeps every block); equal scores are ranked
+    lower j first (the paper does not order ties); no block is forced, the
+    diagonal included. A stable sort of the negated row is the selection step.
+    Returns (mask uint8 [B, H, Nq, Nk], S_c float64 [B, H, Nq, Nk]).
+    """
+    PQ, PK = block_pool(q, block), block_pool(k, block)
+    B, H, nq, _ = PQ.shape
+    nk = PK.shape[2]
+    Sc = np.zeros((B, H, nq, nk))
+    mask = np.zeros((B, H, nq, nk), dtype=np.uint8)
+    for b in range(B):
+        for h in range(H):
+            Sc[b, h] = PQ[b, h] @ PK[b, h].T
+            for i in range(nq):
+                order = np.argsort(-Sc[b, h, i], kind="stable")
+                mask[b, h, i, order[:min(k_keep, nk)]] = 1
+    return mask, Sc

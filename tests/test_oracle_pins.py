@@ -352,3 +352,99 @@ def test_bwd_invariants_sum_dk_zero_sum_dv_equals_sum_do():
     dQ, dK, dV = oracle.bsattn_bwd(q, k, v, do, bm, block, 0.35)
     assert np.allclose(dK.sum(axis=1), 0.0, atol=1e-11)
     assert np.allclose(dV.sum(axis=1), do.sum(axis=1), atol=1e-11)
+
+
+# ---------------------------------------------------------------------------
+# Top-K block selection (Sec. 3.3, Eq. 6 and Eq. 7)
+# ---------------------------------------------------------------------------
+
+def _hand_example():
+    """N = 5 tokens, block 2 (blocks {0,1}, {2,3} and the short {4}), H = 1, D = 2.
+
+    pool(Q): (2,0),(0,2) -> (1,1);  (4,0),(2,2) -> (3,1);  (0,-1) -> (0,-1)
+    pool(K): (2,0),(2,0) -> (2,0);  (0,2),(0,0) -> (0,1);  (2,2)  -> (2,2)
+    S_c = pool(Q) pool(K)^T = [[2, 1, 4], [6, 1, 8], [0, -1, -2]] (worked by hand).
+    Averaging the short block over the block size instead of its one token
+    would give pool(K)_2 = (1,1) and row 0 = [2, 1, 2]; a transposed S_c would
+    give row 0 = [2, 6, 0]: both change the Top-1 answer below.
+    """
+    q = np.array([[2, 0], [0, 2], [4, 0], [2, 2], [0, -1]], dtype=np.float64)
+    k = np.array([[2, 0], [2, 0], [0, 2], [0, 0], [2, 2]], dtype=np.float64)
+    return q.reshape(1, 5, 1, 2), k.reshape(1, 5, 1, 2)
+
+
+def test_topk_hand_worked_example():
+    q, k = _hand_example()
+    mask1, sc = oracle.topk_block_mask(q, k, 2, 1)
+    assert np.array_equal(sc[0, 0], [[2, 1, 4], [6, 1, 8], [0, -1, -2]])
+    assert np.array_equal(mask1[0, 0], [[0, 0, 1], [0, 0, 1], [1, 0, 0]])
+    mask2, _ = oracle.topk_block_mask(q, k, 2, 2)
+    assert np.array_equal(mask2[0, 0], [[1, 0, 1], [1, 0, 1], [1, 1, 0]])
+    mask3, _ = oracle.topk_block_mask(q, k, 2, 3)
+    assert mask3.all()
+
+
+def test_topk_ties_go_to_the_lower_block():
+    # pool(K) equal for blocks 0 and 1 (and 3): every row has an exact tie at its top
+    q = np.ones((1, 8, 1, 2))
+    k = np.array([[1, 0], [1, 0], [0, 1], [1, 0], [0, 0], [0, 0], [1, 0], [0, 1]],
+                 dtype=np.float64).reshape(1, 8, 1, 2)
+    mask, sc = oracle.topk_block_mask(q, k, 2, 1)
+    assert np.array_equal(sc[0, 0, 0], [1, 1, 0, 1])
+    assert np.array_equal(mask[0, 0], np.tile([1, 0, 0, 0], (4, 1)))
+    mask, _ = oracle.topk_block_mask(q, k, 2, 2)
+    assert np.array_equal(mask[0, 0], np.tile([1, 1, 0, 0], (4, 1)))
+
+
+@pytest.mark.parametrize("seed,n,block,H,D,kk", [(1, 37, 8, 2, 4, 2), (2, 64, 16, 1, 3, 1),
+                                                   (3, 50, 8, 3, 5, 4), (4, 9, 4, 1, 2, 5)])
+def test_topk_brute_force(seed, n, block, H, D, kk):
+    """Scalar loops: pooled means token by token, dot products term by term, and
+    the rank definition of Top-K (j is kept iff fewer than kk entries beat it,
+    an entry beating j when larger, or equal with a lower index). Small
+    integer inputs make exact ties common."""
+    rng = np.random.default_rng(seed)
+    q = rng.integers(-2, 3, (1, n, H, D)).astype(np.float64)
+    k = rng.integers(-2, 3, (1, n, H, D)).astype(np.float64)
+    nb = -(-n // block)
+    mask, sc = oracle.topk_block_mask(q, k, block, kk)
+    for h in range(H):
+        pq = [[0.0] * D for _ in range(nb)]
+        pk = [[0.0] * D for _ in range(nb)]
+        for j in range(nb):
+            toks = list(range(j * block, min(n, (j + 1) * block)))
+            for d in range(D):
+                pq[j][d] = sum(q[0, t, h, d] for t in toks) / len(toks)
+                pk[j][d] = sum(k[0, t, h, d] for t in toks) / len(toks)
+        for i in range(nb):
+            row = [sum(pq[i][d] * pk[j][d] for d in range(D)) for j in range(nb)]
+            assert np.allclose(sc[0, h, i], row, rtol=0, atol=1e-12)
+            for j in range(nb):
+                beaten_by = sum(1 for jj in range(nb)
+                                if row[jj] > row[j] or (row[jj] == row[j] and jj < j))
+                assert mask[0, h, i, j] == (1 if beaten_by < kk else 0), (h, i, j)
+
+
+def test_topk_invariants():
+    rng = np.random.default_rng(7)
+    q = rng.standard_normal((2, 300, 3, 16))
+    k = rng.standard_normal((2, 300, 3, 16))
+    block, nb = 32, 10
+    for kk in (1, 3, 9):
+        mask, sc = oracle.topk_block_mask(q, k, block, kk)
+        assert np.all(mask.sum(axis=-1) == kk)
+        # Top-1 is the first maximum (library argmax)
+        if kk == 1:
+            assert np.array_equal(mask.argmax(axis=-1), sc.argmax(axis=-1))
+        # the kept scores are never below a dropped score of the same row
+        lo = np.where(mask == 1, sc, np.inf).min(axis=-1)
+        hi = np.where(mask == 0, sc, -np.inf).max(axis=-1)
+        assert np.all(lo >= hi)
+        # a positive power-of-two scale of Q (exact) changes no selection
+        m4, _ = oracle.topk_block_mask(4.0 * q, k, block, kk)
+        assert np.array_equal(m4, mask)
+    full, _ = oracle.topk_block_mask(q, k, block, nb + 5)
+    assert full.all()
+    # block_pool of a block filled with one vector is that vector, short last block included
+    x = np.repeat(rng.standard_normal((1, 10, 2, 4)), 32, axis=1)[:, :300]
+    assert np.allclose(oracle.block_pool(x, 32)[0, :, :, :].transpose(1, 0, 2), x[0, ::32], atol=1e-12)
