@@ -39,8 +39,8 @@ CAL_COPY_BYTES = 1 << 28      # calibration copy: 256 MiB read + 256 MiB written
 FWD_TRAFFIC = {
     "workload": "c2k_train", "rho": "0.1",
     "read_bytes": 43.862e9, "write_bytes": 0.487e9,
-    "sources": ("bsattn_fwd.hip", "attn_util.h", "common.h"),
-    "sha256": "1fbc8bf030775418ae8d1a1177450c5dcea8c5776a25828dbd0dae571c5f37b8",
+    "sources": ("bsattn_fwd.hip", "attn_util.h"),
+    "sha256": "60b8bec0a3cfc9577a971ffeaa279ebc2aff708e73c8babbc4d306021227e1f8",
 }
 
 
@@ -102,6 +102,35 @@ def cpu_baseline(inst, budget_s: float) -> dict:
             "sample": f"float64 oracle forward+backward, head 0 of 24, query blocks 0..{done - 1} "
                       f"of {nb} ({done / nb / 24:.2%} of the step's attention work), "
                       f"{dt:.1f} s wall"}
+
+
+def time_topk(ut, q, k, blk: int, k_keep: int, stream, reps: int = 10) -> dict:
+    """Top-K block selection (pooling + scores + selection) on the step's Q
+    and K, timed on its own: it is not part of the step, whose block mask is
+    the synthetic one. HBM-bound: it reads Q and K once."""
+    import torch
+    B, N, H, D = q.shape
+    nb = -(-N // blk)
+    mask = torch.empty((B, H, nb, nb), dtype=torch.uint8, device=q.device)
+    ws = torch.empty(ut.ut_topk_block_mask_workspace_size(B, N, H, D, blk), dtype=torch.uint8,
+                     device=q.device)
+    run = lambda: ut.ut_topk_block_mask(q, k, blk, k_keep, mask, ws)
+    for _ in range(2):
+        st = run()
+        if st != ut.UT_OK:
+            raise ut.UltraTexError("ut_topk_block_mask", st, ut.last_error())
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record(stream)
+    for _ in range(reps):
+        run()
+    e1.record(stream)
+    torch.cuda.synchronize()
+    ms = e0.elapsed_time(e1) / reps
+    # Q and K read once, pooled rows written and read back, the mask written
+    nbytes = 2 * B * N * H * D * 2 + 2 * 2 * B * H * nb * D * 4 + B * H * nb * nb
+    return {"ms": round(ms, 4), "k_keep": k_keep, "bytes": nbytes,
+            "gbs": round(nbytes / (ms * 1e-3) / 1e9, 1), "bound": "hbm",
+            "frac_hbm": round(nbytes / (ms * 1e-3) / 1e9 / PEAK_HBM_GBS, 4)}
 
 
 def main():
@@ -237,6 +266,7 @@ def main():
                      "frac": round(fwd_tflops / PEAK_BF16_TFLOPS, 4),
                      "traffic": fwd_traffic(wl.name, wl.rho)},
     }
+    result["topk_mask"] = time_topk(ut, q, k, blk, W.kept_off_diagonal(wl.rho, nb), stream)
     if not args.no_cpu_baseline:
         result["cpu_baseline"] = cpu_baseline(inst, args.cpu_seconds)
     print(json.dumps(result), flush=True)

@@ -185,6 +185,38 @@ ut_status ut_bsattn_bwd(const void* q, const void* k, const void* v,
                         float softmax_scale, void* workspace,
                         size_t workspace_bytes, hipStream_t stream);
 
+/* ------------------------------------------------------------------------
+ * Top-K block selection (Sec. 3.3, Eq. 6 and Eq. 7): the block mask M_c of
+ * block-sparse attention from mean-pooled query and key blocks. Per (b, h),
+ * pool(X)_i is the mean of block i's token rows (a short last block averages
+ * its real tokens), S_c = pool(Q) pool(K)^T, and row i of the mask keeps the
+ * k_keep largest entries of S_c[i, :]. Equal scores are taken lower j first.
+ * No block is forced (the diagonal included). The output feeds
+ * ut_build_block_index.
+ *
+ * q, k        bf16 [B, N, H, D] contiguous, 16-byte aligned.
+ * D           a multiple of 8, at most 512. block: >= 1.
+ * k_keep      blocks kept per row, >= 1 (floor(rho N_k) in the paper; the
+ *             caller computes it); k_keep >= Nk keeps every block.
+ * block_mask  uint8 [B, H, Nk, Nk] output, Nk = ceil(N / block); 1 = kept.
+ * workspace   device scratch of ut_topk_block_mask_workspace_size bytes
+ *             (the pooled rows, fp32), 16-byte aligned.
+ * Scores are fp32 (sums in order over tokens and over d); a row whose
+ * k-th and (k+1)-th scores differ by less than the fp32 rounding of that
+ * arithmetic may differ from an exact-arithmetic selection, and is then still
+ * a valid Top-K of the fp32 scores. Inputs must be finite.
+ * Errors: sizes < 1, D not a multiple of 8 or > 512, B > 65535, null or
+ *         misaligned pointers, k_keep < 1 -> UT_ERR_INVALID_ARG; a row of
+ *         scores too long for one workgroup's LDS (Nk + D > 16384) ->
+ *         UT_ERR_UNSUPPORTED; workspace too small -> UT_ERR_WORKSPACE.
+ * ---------------------------------------------------------------------- */
+size_t ut_topk_block_mask_workspace_size(int32_t B, int32_t N, int32_t H, int32_t D,
+                                         int32_t block);
+ut_status ut_topk_block_mask(const void* q, const void* k, int32_t B, int32_t N,
+                             int32_t H, int32_t D, int32_t block, int32_t k_keep,
+                             uint8_t* block_mask, void* workspace,
+                             size_t workspace_bytes, hipStream_t stream);
+
 #ifdef __cplusplus
 }
 #endif

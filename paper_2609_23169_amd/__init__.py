@@ -31,6 +31,7 @@ EXPORTS = [
     "ut_drop_background_workspace_size", "ut_drop_background",
     "ut_scatter_foreground", "ut_build_block_index",
     "ut_bsattn_fwd", "ut_bsattn_bwd_workspace_size", "ut_bsattn_bwd",
+    "ut_topk_block_mask_workspace_size", "ut_topk_block_mask",
 ]
 
 
@@ -53,6 +54,8 @@ _SIGS = {
     "ut_bsattn_bwd_workspace_size": (_sz, [_i32, _i32, _i32]),
     "ut_bsattn_bwd": (_c.c_int, [_vp, _vp, _vp, _vp, _vp, _vp, _vp, _vp, _vp, _i32, _i32, _i32, _i32, _i32,
                                  _vp, _vp, _vp, _vp, _f32, _vp, _sz, _vp]),
+    "ut_topk_block_mask_workspace_size": (_sz, [_i32, _i32, _i32, _i32, _i32]),
+    "ut_topk_block_mask": (_c.c_int, [_vp, _vp, _i32, _i32, _i32, _i32, _i32, _i32, _vp, _vp, _sz, _vp]),
 }
 
 _lib = None
@@ -207,6 +210,22 @@ def ut_bsattn_bwd(q, k, v, o, dout, lse, dq, dk, dv, block: int, q_rowptr, q_col
                                _p(kv_rows), softmax_scale, _p(workspace), ws_bytes, _stream(stream))
 
 
+def ut_topk_block_mask_workspace_size(B: int, N: int, H: int, D: int, block: int) -> int:
+    return int(lib().ut_topk_block_mask_workspace_size(B, N, H, D, block))
+
+
+def ut_topk_block_mask(q, k, block: int, k_keep: int, block_mask, workspace, stream=None) -> int:
+    _need(q.dim() == 4 and k.shape == q.shape, "q, k: [B, N, H, D], same shape")
+    _need(q.dtype == torch.bfloat16 and k.dtype == torch.bfloat16, "q, k: bf16")
+    B, N, H, D = q.shape
+    nb = -(-N // block)
+    _need(block_mask.dtype == torch.uint8 and block_mask.numel() >= B * H * nb * nb,
+          "block_mask: uint8 [B, H, Nk, Nk]")
+    ws_bytes = _nbytes(workspace) if workspace is not None else 0
+    return lib().ut_topk_block_mask(_p(q), _p(k), B, N, H, D, block, k_keep, _p(block_mask),
+                                    _p(workspace), ws_bytes, _stream(stream))
+
+
 # ---------------------------------------------------------------------------
 # Allocating helpers (raise on error)
 # ---------------------------------------------------------------------------
@@ -279,3 +298,15 @@ def bsattn_bwd(q, k, v, o, dout, lse, index, block: int, softmax_scale: float, w
                                           index["q_rowptr"], index["q_cols"], index["kv_colptr"],
                                           index["kv_rows"], softmax_scale, workspace, stream))
     return dq, dk, dv
+
+
+def topk_block_mask(q, k, block: int, k_keep: int, workspace=None, stream=None):
+    """Block mask [B, H, Nk, Nk] uint8 of the k_keep best key blocks per query block."""
+    B, N, H, D = q.shape
+    nb = -(-N // block)
+    mask = torch.empty((B, H, nb, nb), dtype=torch.uint8, device=q.device)
+    if workspace is None:
+        workspace = torch.empty(max(ut_topk_block_mask_workspace_size(B, N, H, D, block), 16),
+                                dtype=torch.uint8, device=q.device)
+    _raise("ut_topk_block_mask", ut_topk_block_mask(q, k, block, k_keep, mask, workspace, stream))
+    return mask

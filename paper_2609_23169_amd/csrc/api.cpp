@@ -224,4 +224,43 @@ ut_status ut_bsattn_bwd(const void* q, const void* k, const void* v, const void*
                    "backward launch");
 }
 
+size_t ut_topk_block_mask_workspace_size(int32_t B, int32_t N, int32_t H, int32_t D,
+                                         int32_t block) {
+  if (B < 1 || N < 1 || H < 1 || D < 1 || block < 1) return 0;
+  const int64_t nblk = ((int64_t)N + block - 1) / block;
+  return (size_t)2 * B * H * nblk * D * sizeof(float);   // pooled Q and K
+}
+
+ut_status ut_topk_block_mask(const void* q, const void* k, int32_t B, int32_t N, int32_t H,
+                             int32_t D, int32_t block, int32_t k_keep, uint8_t* block_mask,
+                             void* workspace, size_t workspace_bytes, hipStream_t stream) {
+  static const char* fn = "ut_topk_block_mask";
+  g_last_error[0] = 0;
+  if (B < 1 || N < 1 || H < 1 || block < 1)
+    return fail(UT_ERR_INVALID_ARG, "%s: B, N, H, block must be >= 1 (got %d, %d, %d, %d)", fn,
+                B, N, H, block);
+  if (D < 8 || D > 512 || D % 8 != 0)
+    return fail(UT_ERR_INVALID_ARG, "%s: head_dim must be a multiple of 8 in [8, 512] (got %d)",
+                fn, D);
+  if (B > 65535) return fail(UT_ERR_INVALID_ARG, "%s: B must be <= 65535 (got %d)", fn, B);
+  if (k_keep < 1) return fail(UT_ERR_INVALID_ARG, "%s: k_keep must be >= 1 (got %d)", fn, k_keep);
+  const int64_t nblk = ((int64_t)N + block - 1) / block;
+  if ((int64_t)B * N * H * D >= (int64_t)1 << 40 || (int64_t)B * H * nblk >= (int64_t)1 << 31)
+    return fail(UT_ERR_INVALID_ARG, "%s: problem too large", fn);
+  if (topk_rows_per_group(D, (int)nblk) == 0)
+    return fail(UT_ERR_UNSUPPORTED, "%s: %lld blocks per row do not fit one workgroup", fn,
+                (long long)nblk);
+  UT_TRY(check_ptr(fn, "q", q, 16));
+  UT_TRY(check_ptr(fn, "k", k, 16));
+  UT_TRY(check_ptr(fn, "block_mask", block_mask, 1));
+  const size_t need = ut_topk_block_mask_workspace_size(B, N, H, D, block);
+  if (!workspace || workspace_bytes < need)
+    return fail(UT_ERR_WORKSPACE, "%s: workspace of %zu bytes required (got %zu)", fn, need,
+                workspace ? workspace_bytes : (size_t)0);
+  UT_TRY(check_ptr(fn, "workspace", workspace, 16));
+  return check_hip(launch_topk_block_mask(q, k, B, N, H, D, block, k_keep, block_mask,
+                                          static_cast<float*>(workspace), stream),
+                   "top-k launch");
+}
+
 }  // extern "C"

@@ -43,4 +43,12 @@ hipError_t launch_bsattn_bwd(const void* q, const void* k, const void* v, const 
                              const int32_t* colptr, const int32_t* rows, float* delta,
                              hipStream_t s);
 
+// ---- Top-K block selection (topk_mask.hip) ----
+constexpr int64_t kTopkMaxLds = 65536;   // LDS bytes of one selection workgroup
+// Query blocks per selection workgroup (16, 4 or 1), 0 if one row does not fit.
+int topk_rows_per_group(int D, int nblk);
+hipError_t launch_topk_block_mask(const void* q, const void* k, int B, int N, int H, int D,
+                                  int block, int k_keep, uint8_t* mask, float* pooled,
+                                  hipStream_t s);
+
 }  // namespace ut

@@ -62,3 +62,57 @@ def block_rows(blocks, block, n):
 
 def scale_of(d):
     return 1.0 / math.sqrt(d)
+
+
+# ---------------------------------------------------------------------------
+# Top-K block masks: fp32 scores against the exact (float64) selection
+# ---------------------------------------------------------------------------
+U32 = 2.0 ** -24
+
+
+def _gamma(n):
+    return n * U32 / (1 - n * U32)
+
+
+def topk_tolerance(q, k, block):
+    """Bound on |S_c(fp32) - S_c(exact)| per entry, for any summation order.
+
+    A pooled entry sums at most `block` exact bf16 values in fp32 and divides
+    once: |error| <= gamma_block * mean_t |x_td| + u |pool_d|. The fp32 dot
+    product over D terms adds gamma_D sum_d |pq_d pk_d|. The first-order sum
+    of these is doubled to cover the second-order terms.
+    """
+    import oracle
+    PQ, PK = np.abs(oracle.block_pool(q, block)), np.abs(oracle.block_pool(k, block))
+    AQ = oracle.block_pool(np.abs(to_np64(q)), block)
+    AK = oracle.block_pool(np.abs(to_np64(k)), block)
+    D = PQ.shape[-1]
+    g = _gamma(block)
+    mm = lambda a, b: a @ np.swapaxes(b, -1, -2)
+    return 2.0 * (g * (mm(AQ, PK) + mm(PQ, AK)) + (2 * U32 + _gamma(D)) * mm(PQ, PK))
+
+
+def to_np64(t):
+    return t.detach().to(torch.float64).cpu().numpy() if isinstance(t, torch.Tensor) else np.asarray(t, np.float64)
+
+
+def check_topk(mask_gpu, ref_mask, scores, tol, k_keep, label=""):
+    """Every GPU row keeps min(k_keep, Nk) blocks and is a Top-K of the exact
+    scores within `tol`; rows whose exact selection is decided by more than
+    the tolerance match the oracle exactly. Returns the decided fraction."""
+    m = to_np(mask_gpu).astype(np.uint8) if isinstance(mask_gpu, torch.Tensor) else mask_gpu
+    nk = m.shape[-1]
+    assert set(np.unique(m)) <= {0, 1}, f"{label} mask values {np.unique(m)}"
+    assert np.all(m.sum(-1) == min(k_keep, nk)), f"{label} row counts"
+    if k_keep >= nk:
+        assert m.all()
+        return 1.0
+    sel, ref = m.astype(bool), ref_mask.astype(bool)
+    lo = np.where(sel, scores + tol, np.inf).min(-1)
+    hi = np.where(~sel, scores - tol, -np.inf).max(-1)
+    bad = lo < hi
+    assert not bad.any(), f"{label} {int(bad.sum())} rows are not a Top-K within the fp32 bound"
+    decided = np.where(ref, scores - tol, np.inf).min(-1) > np.where(~ref, scores + tol, -np.inf).max(-1)
+    diff = (sel != ref).any(-1) & decided
+    assert not diff.any(), f"{label} {int(diff.sum())} decided rows differ from the oracle"
+    return float(decided.mean())

@@ -111,3 +111,31 @@ def test_binding_refuses_host_tensors():
     idx = torch.zeros(2, dtype=torch.int32)
     with pytest.raises(ValueError):
         ut.ut_bsattn_fwd(q, q, q, q, torch.zeros(64), 64, idx, idx, 0.125)
+
+
+def test_topk_block_mask_rejects_bad_arguments():
+    lib = ut.lib()
+    assert ut.ut_topk_block_mask_workspace_size(1, 77060, 24, 128, 128) == 2 * 24 * 603 * 128 * 4
+    assert ut.ut_topk_block_mask_workspace_size(1, 0, 24, 128, 128) == 0
+    ws = ut.ut_topk_block_mask_workspace_size(1, 1000, 2, 64, 64)
+    call = lambda **kw: lib.ut_topk_block_mask(
+        kw.get("q", FAKE), kw.get("k", FAKE), kw.get("B", 1), kw.get("N", 1000), kw.get("H", 2),
+        kw.get("D", 64), kw.get("block", 64), kw.get("kk", 3), kw.get("m", FAKE),
+        kw.get("ws", FAKE), kw.get("wsb", ws), None)
+    for kw, status, msg in [
+        (dict(N=0), ut.UT_ERR_INVALID_ARG, ">= 1"),
+        (dict(block=0), ut.UT_ERR_INVALID_ARG, ">= 1"),
+        (dict(D=60), ut.UT_ERR_INVALID_ARG, "multiple of 8"),
+        (dict(D=520), ut.UT_ERR_INVALID_ARG, "multiple of 8"),
+        (dict(kk=0), ut.UT_ERR_INVALID_ARG, "k_keep"),
+        (dict(B=70000), ut.UT_ERR_INVALID_ARG, "65535"),
+        (dict(q=None), ut.UT_ERR_INVALID_ARG, "q is NULL"),
+        (dict(k=MISALIGNED), ut.UT_ERR_INVALID_ARG, "aligned"),
+        (dict(m=None), ut.UT_ERR_INVALID_ARG, "block_mask is NULL"),
+        (dict(ws=None), ut.UT_ERR_WORKSPACE, "workspace"),
+        (dict(wsb=ws - 1), ut.UT_ERR_WORKSPACE, "workspace"),
+        # 20000 blocks of one token: a score row of 80 KB does not fit one workgroup
+        (dict(N=20000, block=1, wsb=1 << 40), ut.UT_ERR_UNSUPPORTED, "do not fit"),
+    ]:
+        assert call(**kw) == status, kw
+        assert msg in ut.last_error(), (kw, ut.last_error())
