@@ -18,6 +18,10 @@ Paper sections (arXiv 2609.23169, "UltraTex"):
   * Block-Sparse Attention: Sec. 3.3, Eq. 5 (dense softmax attention with
     scale 1/sqrt(d)), the b_q / b_kv block partition, Eq. 7 (binary block mask
     M_c) and Eq. 8 (each query block attends only to its selected key blocks).
+  * Foreground-restricted training and sampling: Sec. 3.2, Eq. 3 (the flow
+    matching loss over the gathered foreground target tokens, with the target
+    velocity eps - z_tgt of Eq. 1-2) and Eq. 4 (the Euler step applied only
+    at the retained positions).
   * Top-K block selection: Sec. 3.3, Eq. 6 (compressed scores from
     mean-pooled query and key blocks) and Eq. 7 (row-wise Top-K over the key
     blocks gives the block mask).
@@ -34,6 +38,7 @@ __all__ = [
     "compact", "gather", "scatter", "block_index",
     "bsattn_fwd", "bsattn_bwd",
     "block_pool", "topk_block_mask",
+    "euler_update_fg", "fg_flow_loss",
 ]
 
 
@@ -264,3 +269,41 @@ def topk_block_mask(q, k, block: int, k_keep: int):
                 order = np.argsort(-Sc[b, h, i], kind="stable")
                 mask[b, h, i, order[:min(k_keep, nk)]] = 1
     return mask, Sc
+
+
+# ---------------------------------------------------------------------------
+# Foreground-restricted sampling and training (Sec. 3.2, Eq. 3 and Eq. 4)
+# ---------------------------------------------------------------------------
+
+def euler_update_fg(z, v, kept_idx, dt: float) -> np.ndarray:
+    """Eq. 4: z_i <- z_i + (t_prev - t_curr) v_i for every retained position i;
+    every other position keeps its value (the initial noise).
+
+    z [L, C] full-grid latent, v [n, C] packed velocities (row k belongs to
+    position kept_idx[k]), dt = t_prev - t_curr. Returns the new z in float64.
+    """
+    Z = _f64(z).copy()
+    V = _f64(v)
+    for k, i in enumerate(np.asarray(kept_idx).tolist()):
+        Z[i, :] = Z[i, :] + dt * V[k, :]
+    return Z
+
+
+def fg_flow_loss(v, eps, z0, kept_idx):
+    """Eq. 3: the flow matching loss over the foreground target tokens only,
+    || v_hat - Gather_{M_fg}(eps - z_tgt) ||^2, with the target velocity
+    eps - z_tgt of Eq. 1-2.
+
+    Reading: the squared norm is averaged over the n retained tokens and the
+    C channels (a mean squared error; the paper writes the norm inside an
+    expectation and fixes no normalisation). Returns (loss, grad) with
+    grad = d loss / d v_hat = 2 (v_hat - target) / (n C), float64.
+    """
+    V, E, Z = _f64(v), _f64(eps), _f64(z0)
+    idx = np.asarray(kept_idx).tolist()
+    n, C = V.shape
+    target = np.stack([E[i, :] - Z[i, :] for i in idx]) if n else np.zeros((0, C))
+    diff = V - target
+    loss = float((diff * diff).sum() / (n * C)) if n else 0.0
+    grad = 2.0 * diff / (n * C) if n else np.zeros((0, C))
+    return loss, grad

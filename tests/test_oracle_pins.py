@@ -448,3 +448,72 @@ def test_topk_invariants():
     # block_pool of a block filled with one vector is that vector, short last block included
     x = np.repeat(rng.standard_normal((1, 10, 2, 4)), 32, axis=1)[:, :300]
     assert np.allclose(oracle.block_pool(x, 32)[0, :, :, :].transpose(1, 0, 2), x[0, ::32], atol=1e-12)
+
+
+# ---------------------------------------------------------------------------
+# Foreground-restricted sampling and training (Sec. 3.2, Eq. 3 and Eq. 4)
+# ---------------------------------------------------------------------------
+
+def test_euler_hand_example_and_untouched_background():
+    # L = 4 positions, C = 2, positions 1 and 3 retained; dt = t_prev - t_curr = -0.25
+    z = np.array([[1.0, 2.0], [3.0, 4.0], [5.0, 6.0], [7.0, 8.0]])
+    v = np.array([[4.0, -8.0], [2.0, 0.0]])
+    out = oracle.euler_update_fg(z, v, np.array([1, 3]), -0.25)
+    assert np.array_equal(out, [[1, 2], [2, 6], [5, 6], [6.5, 8]])
+    assert np.array_equal(z, [[1, 2], [3, 4], [5, 6], [7, 8]])   # input not modified
+
+
+def test_euler_composes_and_matches_torch_index_add():
+    rng = np.random.default_rng(3)
+    L, C = 500, 16
+    z = rng.standard_normal((L, C))
+    mask = rng.random(L) < 0.4
+    kept = np.flatnonzero(mask)
+    v1, v2 = rng.standard_normal((kept.size, C)), rng.standard_normal((kept.size, C))
+    # two steps = one step with the combined increment (exact here up to rounding)
+    two = oracle.euler_update_fg(oracle.euler_update_fg(z, v1, kept, 0.5), v2, kept, -0.125)
+    ref = torch.from_numpy(z).index_add(0, torch.from_numpy(kept), torch.from_numpy(0.5 * v1 - 0.125 * v2))
+    assert np.allclose(two, ref.numpy(), rtol=0, atol=1e-12)
+    assert np.array_equal(two[~mask], z[~mask])
+    assert np.array_equal(oracle.euler_update_fg(z, v1, kept, 0.0), z)
+
+
+def test_fg_loss_hand_example():
+    # two retained positions (2 and 0) of L = 3, C = 2
+    eps = np.array([[1.0, 1.0], [9.0, 9.0], [3.0, 0.0]])
+    z0 = np.array([[0.5, 2.0], [9.0, 9.0], [1.0, 1.0]])
+    kept = np.array([2, 0])
+    # targets eps - z0: row 2 -> (2, -1), row 0 -> (0.5, -1)
+    v = np.array([[3.0, -1.0], [0.5, 1.0]])
+    loss, grad = oracle.fg_flow_loss(v, eps, z0, kept)
+    # diffs (1, 0) and (0, 2): sum of squares 5 over n C = 4
+    assert loss == 5.0 / 4.0
+    assert np.array_equal(grad, [[0.5, 0.0], [0.0, 1.0]])
+
+
+def test_fg_loss_matches_mse_and_finite_differences():
+    rng = np.random.default_rng(4)
+    L, C = 300, 8
+    eps, z0 = rng.standard_normal((L, C)), rng.standard_normal((L, C))
+    kept = np.flatnonzero(rng.random(L) < 0.5)
+    v = rng.standard_normal((kept.size, C))
+    loss, grad = oracle.fg_flow_loss(v, eps, z0, kept)
+    target = torch.from_numpy(eps[kept] - z0[kept])
+    vt = torch.from_numpy(v).requires_grad_(True)
+    ref = torch.nn.functional.mse_loss(vt, target)
+    ref.backward()
+    assert abs(loss - ref.item()) <= 1e-12 * max(1.0, ref.item())
+    assert np.allclose(grad, vt.grad.numpy(), rtol=0, atol=1e-15)
+    # central differences on a few entries
+    h = 1e-6
+    for k, c in [(0, 0), (3, 5), (kept.size - 1, C - 1)]:
+        vp, vm = v.copy(), v.copy()
+        vp[k, c] += h
+        vm[k, c] -= h
+        fd = (oracle.fg_flow_loss(vp, eps, z0, kept)[0] - oracle.fg_flow_loss(vm, eps, z0, kept)[0]) / (2 * h)
+        assert abs(fd - grad[k, c]) <= 1e-8
+    # the exact velocity gives zero loss; background rows never matter
+    assert oracle.fg_flow_loss(eps[kept] - z0[kept], eps, z0, kept)[0] == 0.0
+    eps2 = eps.copy()
+    eps2[np.setdiff1d(np.arange(L), kept)] = np.nan
+    assert oracle.fg_flow_loss(v, eps2, z0, kept)[0] == loss
