@@ -133,6 +133,42 @@ def time_topk(ut, q, k, blk: int, k_keep: int, stream, reps: int = 10) -> dict:
             "frac_hbm": round(nbytes / (ms * 1e-3) / 1e9 / PEAK_HBM_GBS, 4)}
 
 
+def time_fg_step(ut, fg_mask, grid: int, dev, stream, C: int = 64, reps: int = 20) -> dict:
+    """The foreground-only Euler update (Eq. 4) and flow-matching loss with
+    gradient (Eq. 3) on the six target views' latent grid (6 x grid^2 tokens,
+    64 latent channels), timed on their own: HBM-bound row gathers."""
+    import numpy as np
+    import torch
+    L = 6 * grid * grid
+    kept = torch.from_numpy(np.flatnonzero(fg_mask[:L]).astype(np.int32)).to(dev)
+    n = kept.numel()
+    g = torch.Generator(device=dev).manual_seed(5)
+    z = torch.randn((L, C), device=dev, generator=g)
+    eps = torch.randn((L, C), device=dev, generator=g)
+    v = torch.randn((n, C), device=dev, generator=g).to(torch.bfloat16)
+    loss = torch.empty(1, dtype=torch.float32, device=dev)
+    grad = torch.empty((n, C), dtype=torch.float32, device=dev)
+    ws = torch.empty(ut.ut_fg_flow_loss_workspace_size(), dtype=torch.uint8, device=dev)
+    out = {"tokens": L, "kept": n, "channels": C}
+    for name, run, nbytes in (
+            ("euler", lambda: ut.ut_euler_update_foreground(z, v, kept, n, -1.0 / 28),
+             n * C * 2 + 2 * n * C * 4 + 4 * n),
+            ("loss", lambda: ut.ut_fg_flow_loss(v, eps, z, kept, n, loss, grad, ws),
+             n * C * 2 + 3 * n * C * 4 + 4 * n)):
+        st = run()
+        if st != ut.UT_OK:
+            raise ut.UltraTexError(name, st, ut.last_error())
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record(stream)
+        for _ in range(reps):
+            run()
+        e1.record(stream)
+        torch.cuda.synchronize()
+        ms = e0.elapsed_time(e1) / reps
+        out[name] = {"ms": round(ms, 4), "bytes": nbytes, "gbs": round(nbytes / (ms * 1e-3) / 1e9, 1)}
+    return out
+
+
 def main():
     args = parse()
     if args.gpus != 1:
@@ -267,6 +303,7 @@ def main():
                      "traffic": fwd_traffic(wl.name, wl.rho)},
     }
     result["topk_mask"] = time_topk(ut, q, k, blk, W.kept_off_diagonal(wl.rho, nb), stream)
+    result["fg_step"] = time_fg_step(ut, inst.fg_mask, wl.grid, dev, stream)
     if not args.no_cpu_baseline:
         result["cpu_baseline"] = cpu_baseline(inst, args.cpu_seconds)
     print(json.dumps(result), flush=True)

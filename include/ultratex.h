@@ -47,6 +47,12 @@ typedef enum {
   UT_ERR_HIP = 5          /* a HIP runtime or launch error                  */
 } ut_status;
 
+/* Element types of the foreground step calls. */
+typedef enum {
+  UT_BF16 = 0,
+  UT_F32 = 1
+} ut_dtype;
+
 /* Message for the last non-OK status returned on this thread ("" if none). */
 const char* ut_last_error(void);
 
@@ -216,6 +222,53 @@ ut_status ut_topk_block_mask(const void* q, const void* k, int32_t B, int32_t N,
                              int32_t H, int32_t D, int32_t block, int32_t k_keep,
                              uint8_t* block_mask, void* workspace,
                              size_t workspace_bytes, hipStream_t stream);
+
+/* ------------------------------------------------------------------------
+ * Foreground-only Euler update (Sec. 3.2, Eq. 4): at every retained position
+ * i = kept_idx[k], z[i, :] += dt * v[k, :] with dt = t_prev - t_curr; all
+ * other positions keep their values (the initial noise).
+ *
+ * z         fp32 [L, C] in/out, 16-byte aligned.
+ * v         [n_kept, C] packed velocities, UT_BF16 or UT_F32, aligned to
+ *           8 (bf16) or 16 (fp32) bytes.
+ * C         channels per token, a positive multiple of 4.
+ * kept_idx  [n_kept] int32, distinct positions (as ut_drop_background
+ *           produces); entries outside [0, L) are skipped.
+ * Each element is one fp32 fused multiply-add (one rounding). n_kept = 0 is
+ * a no-op.
+ * Errors: L < 1, C not a positive multiple of 4, n_kept < 0 or > L, bad
+ *         dtype, non-finite dt, null or misaligned pointers ->
+ *         UT_ERR_INVALID_ARG.
+ * ---------------------------------------------------------------------- */
+ut_status ut_euler_update_foreground(float* z, int64_t L, int64_t C, const void* v,
+                                     ut_dtype v_dtype, const int32_t* kept_idx,
+                                     int64_t n_kept, float dt, hipStream_t stream);
+
+/* ------------------------------------------------------------------------
+ * Foreground flow-matching loss (Sec. 3.2, Eq. 3, with the target velocity
+ * eps - z_tgt of Eq. 1-2): with i = kept_idx[k],
+ *   loss = sum_{k, c} (v[k, c] - (eps[i, c] - z0[i, c]))^2 / (n_kept C)
+ * (the mean over retained tokens and channels), and optionally its gradient
+ *   grad[k, c] = 2 (v[k, c] - (eps[i, c] - z0[i, c])) / (n_kept C).
+ *
+ * v         [n_kept, C] model prediction, v_dtype.
+ * eps, z0   [L, C] noise and clean target latent on the full grid, x_dtype.
+ *           Rows not listed in kept_idx are never read.
+ * loss      [1] fp32 device output (0 when n_kept = 0).
+ * grad      [n_kept, C] fp32 device output, or NULL.
+ * workspace device scratch of ut_fg_flow_loss_workspace_size() bytes,
+ *           8-byte aligned (per-workgroup partial sums).
+ * Differences and squares are taken in fp64 and summed in a fixed order: the
+ * loss is deterministic and within a few fp64 roundings of exact before its
+ * final rounding to fp32. Alignment as for ut_euler_update_foreground.
+ * Errors: as ut_euler_update_foreground, plus UT_ERR_WORKSPACE.
+ * ---------------------------------------------------------------------- */
+size_t ut_fg_flow_loss_workspace_size(void);
+ut_status ut_fg_flow_loss(const void* v, ut_dtype v_dtype, const void* eps, const void* z0,
+                          ut_dtype x_dtype, int64_t L, int64_t C,
+                          const int32_t* kept_idx, int64_t n_kept, float* loss,
+                          float* grad, void* workspace, size_t workspace_bytes,
+                          hipStream_t stream);
 
 #ifdef __cplusplus
 }

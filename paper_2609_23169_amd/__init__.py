@@ -22,6 +22,7 @@ HERE = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(HERE, "libultratex.so")
 
 UT_OK, UT_ERR_INVALID_ARG, UT_ERR_UNSUPPORTED, UT_ERR_WORKSPACE, UT_ERR_CAPACITY, UT_ERR_HIP = range(6)
+UT_BF16, UT_F32 = 0, 1
 STATUS_NAMES = ["UT_OK", "UT_ERR_INVALID_ARG", "UT_ERR_UNSUPPORTED", "UT_ERR_WORKSPACE",
                 "UT_ERR_CAPACITY", "UT_ERR_HIP"]
 
@@ -32,6 +33,7 @@ EXPORTS = [
     "ut_scatter_foreground", "ut_build_block_index",
     "ut_bsattn_fwd", "ut_bsattn_bwd_workspace_size", "ut_bsattn_bwd",
     "ut_topk_block_mask_workspace_size", "ut_topk_block_mask",
+    "ut_euler_update_foreground", "ut_fg_flow_loss_workspace_size", "ut_fg_flow_loss",
 ]
 
 
@@ -56,6 +58,10 @@ _SIGS = {
                                  _vp, _vp, _vp, _vp, _f32, _vp, _sz, _vp]),
     "ut_topk_block_mask_workspace_size": (_sz, [_i32, _i32, _i32, _i32, _i32]),
     "ut_topk_block_mask": (_c.c_int, [_vp, _vp, _i32, _i32, _i32, _i32, _i32, _i32, _vp, _vp, _sz, _vp]),
+    "ut_euler_update_foreground": (_c.c_int, [_vp, _i64, _i64, _vp, _c.c_int, _vp, _i64, _f32, _vp]),
+    "ut_fg_flow_loss_workspace_size": (_sz, []),
+    "ut_fg_flow_loss": (_c.c_int, [_vp, _c.c_int, _vp, _vp, _c.c_int, _i64, _i64, _vp, _i64, _vp, _vp,
+                                   _vp, _sz, _vp]),
 }
 
 _lib = None
@@ -226,6 +232,40 @@ def ut_topk_block_mask(q, k, block: int, k_keep: int, block_mask, workspace, str
                                     _p(workspace), ws_bytes, _stream(stream))
 
 
+def _dtype_code(t) -> int:
+    if t.dtype == torch.bfloat16:
+        return UT_BF16
+    _need(t.dtype == torch.float32, "tensors must be bf16 or fp32")
+    return UT_F32
+
+
+def ut_euler_update_foreground(z, v, kept_idx, n_kept: int, dt: float, stream=None) -> int:
+    _need(z.dtype == torch.float32 and z.dim() == 2, "z: fp32 [L, C]")
+    L, C = z.shape
+    _need(v.dim() == 2 and v.shape[1] == C and v.shape[0] >= n_kept, "v: [n_kept, C]")
+    _need(kept_idx.dtype == torch.int32 and kept_idx.numel() >= n_kept, "kept_idx: int32 [n_kept]")
+    return lib().ut_euler_update_foreground(_p(z), L, C, _p(v), _dtype_code(v), _p(kept_idx),
+                                            n_kept, dt, _stream(stream))
+
+
+def ut_fg_flow_loss_workspace_size() -> int:
+    return int(lib().ut_fg_flow_loss_workspace_size())
+
+
+def ut_fg_flow_loss(v, eps, z0, kept_idx, n_kept: int, loss, grad, workspace, stream=None) -> int:
+    _need(eps.dim() == 2 and z0.shape == eps.shape and z0.dtype == eps.dtype, "eps, z0: [L, C], same dtype")
+    L, C = eps.shape
+    _need(v.dim() == 2 and v.shape[1] == C and v.shape[0] >= n_kept, "v: [n_kept, C]")
+    _need(kept_idx.dtype == torch.int32 and kept_idx.numel() >= n_kept, "kept_idx: int32 [n_kept]")
+    _need(loss.dtype == torch.float32 and loss.numel() >= 1, "loss: fp32 [1]")
+    if grad is not None:
+        _need(grad.dtype == torch.float32 and grad.numel() >= n_kept * C, "grad: fp32 [n_kept, C]")
+    ws_bytes = _nbytes(workspace) if workspace is not None else 0
+    return lib().ut_fg_flow_loss(_p(v), _dtype_code(v), _p(eps), _p(z0), _dtype_code(eps), L, C,
+                                 _p(kept_idx), n_kept, _p(loss), _p(grad) if grad is not None else None,
+                                 _p(workspace), ws_bytes, _stream(stream))
+
+
 # ---------------------------------------------------------------------------
 # Allocating helpers (raise on error)
 # ---------------------------------------------------------------------------
@@ -310,3 +350,21 @@ def topk_block_mask(q, k, block: int, k_keep: int, workspace=None, stream=None):
                                 dtype=torch.uint8, device=q.device)
     _raise("ut_topk_block_mask", ut_topk_block_mask(q, k, block, k_keep, mask, workspace, stream))
     return mask
+
+
+def euler_update_foreground(z, v, kept_idx, dt: float, stream=None):
+    """In place: z[kept_idx[k]] += dt * v[k] (Eq. 4). Returns z."""
+    _raise("ut_euler_update_foreground",
+           ut_euler_update_foreground(z, v, kept_idx, kept_idx.numel(), dt, stream))
+    return z
+
+
+def fg_flow_loss(v, eps, z0, kept_idx, with_grad: bool = True, workspace=None, stream=None):
+    """(loss [1] fp32, grad [n, C] fp32 or None) of Eq. 3 on the device."""
+    n, C = kept_idx.numel(), eps.shape[1]
+    loss = torch.empty(1, dtype=torch.float32, device=eps.device)
+    grad = torch.empty((n, C), dtype=torch.float32, device=eps.device) if with_grad else None
+    if workspace is None:
+        workspace = torch.empty(ut_fg_flow_loss_workspace_size(), dtype=torch.uint8, device=eps.device)
+    _raise("ut_fg_flow_loss", ut_fg_flow_loss(v, eps, z0, kept_idx, n, loss, grad, workspace, stream))
+    return loss, grad

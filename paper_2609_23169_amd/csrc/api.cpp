@@ -263,4 +263,65 @@ ut_status ut_topk_block_mask(const void* q, const void* k, int32_t B, int32_t N,
                    "top-k launch");
 }
 
+namespace {
+ut_status check_fg_common(const char* fn, int64_t L, int64_t C, int64_t n, const void* v,
+                          ut_dtype vt) {
+  if (L < 1 || L >= ((int64_t)1 << 31))
+    return fail(UT_ERR_INVALID_ARG, "%s: L must be in [1, 2^31) (got %lld)", fn, (long long)L);
+  if (C < 4 || C % 4 != 0 || C > (1 << 20))
+    return fail(UT_ERR_INVALID_ARG, "%s: C must be a positive multiple of 4 (got %lld)", fn,
+                (long long)C);
+  if (n < 0 || n > L)
+    return fail(UT_ERR_INVALID_ARG, "%s: n_kept must be in [0, L] (got %lld)", fn, (long long)n);
+  if (vt != UT_BF16 && vt != UT_F32)
+    return fail(UT_ERR_INVALID_ARG, "%s: unknown dtype %d", fn, (int)vt);
+  if (n > 0) UT_TRY(check_ptr(fn, "v", v, vt == UT_BF16 ? 8 : 16));
+  return UT_OK;
+}
+}  // namespace
+
+ut_status ut_euler_update_foreground(float* z, int64_t L, int64_t C, const void* v,
+                                     ut_dtype v_dtype, const int32_t* kept_idx,
+                                     int64_t n_kept, float dt, hipStream_t stream) {
+  static const char* fn = "ut_euler_update_foreground";
+  g_last_error[0] = 0;
+  UT_TRY(check_fg_common(fn, L, C, n_kept, v, v_dtype));
+  if (!std::isfinite(dt)) return fail(UT_ERR_INVALID_ARG, "%s: dt must be finite", fn);
+  if (n_kept == 0) return UT_OK;
+  UT_TRY(check_ptr(fn, "z", z, 16));
+  UT_TRY(check_ptr(fn, "kept_idx", kept_idx, 4));
+  return check_hip(launch_euler_fg(z, L, C, v, v_dtype == UT_BF16, kept_idx, n_kept, dt, stream),
+                   "euler launch");
+}
+
+size_t ut_fg_flow_loss_workspace_size(void) { return (size_t)kLossParts * sizeof(double); }
+
+ut_status ut_fg_flow_loss(const void* v, ut_dtype v_dtype, const void* eps, const void* z0,
+                          ut_dtype x_dtype, int64_t L, int64_t C, const int32_t* kept_idx,
+                          int64_t n_kept, float* loss, float* grad, void* workspace,
+                          size_t workspace_bytes, hipStream_t stream) {
+  static const char* fn = "ut_fg_flow_loss";
+  g_last_error[0] = 0;
+  UT_TRY(check_fg_common(fn, L, C, n_kept, v, v_dtype));
+  if (x_dtype != UT_BF16 && x_dtype != UT_F32)
+    return fail(UT_ERR_INVALID_ARG, "%s: unknown dtype %d", fn, (int)x_dtype);
+  UT_TRY(check_ptr(fn, "loss", loss, 4));
+  if (n_kept > 0) {
+    const uintptr_t xa = x_dtype == UT_BF16 ? 8 : 16;
+    UT_TRY(check_ptr(fn, "eps", eps, xa));
+    UT_TRY(check_ptr(fn, "z0", z0, xa));
+    UT_TRY(check_ptr(fn, "kept_idx", kept_idx, 4));
+    if (grad) UT_TRY(check_ptr(fn, "grad", grad, 16));
+  }
+  const size_t need = ut_fg_flow_loss_workspace_size();
+  if (!workspace || workspace_bytes < need)
+    return fail(UT_ERR_WORKSPACE, "%s: workspace of %zu bytes required (got %zu)", fn, need,
+                workspace ? workspace_bytes : (size_t)0);
+  UT_TRY(check_ptr(fn, "workspace", workspace, 8));
+  return check_hip(launch_fg_loss(v, v_dtype == UT_BF16, eps, z0, x_dtype == UT_BF16, L, C,
+                                  kept_idx, n_kept, loss, grad, static_cast<double*>(workspace),
+                                  stream),
+                   "loss launch");
+}
+
 }  // extern "C"

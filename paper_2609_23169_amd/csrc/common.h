@@ -51,4 +51,12 @@ hipError_t launch_topk_block_mask(const void* q, const void* k, int B, int N, in
                                   int block, int k_keep, uint8_t* mask, float* pooled,
                                   hipStream_t s);
 
+// ---- Foreground Euler update and loss (fg_step.hip) ----
+constexpr int kLossParts = 1024;   // partial sums of the loss (fixed order)
+hipError_t launch_euler_fg(float* z, int64_t L, int64_t C, const void* v, bool v_bf16,
+                           const int32_t* kept, int64_t n, float dt, hipStream_t s);
+hipError_t launch_fg_loss(const void* v, bool v_bf16, const void* eps, const void* z0,
+                          bool x_bf16, int64_t L, int64_t C, const int32_t* kept, int64_t n,
+                          float* loss, float* grad, double* partial, hipStream_t s);
+
 }  // namespace ut

@@ -139,3 +139,32 @@ def test_topk_block_mask_rejects_bad_arguments():
     ]:
         assert call(**kw) == status, kw
         assert msg in ut.last_error(), (kw, ut.last_error())
+
+
+def test_foreground_step_calls_reject_bad_arguments():
+    lib = ut.lib()
+    assert ut.ut_fg_flow_loss_workspace_size() == 1024 * 8
+    eu = lambda **kw: lib.ut_euler_update_foreground(
+        kw.get("z", FAKE), kw.get("L", 1000), kw.get("C", 64), kw.get("v", FAKE), kw.get("vt", ut.UT_BF16),
+        kw.get("kept", FAKE), kw.get("n", 10), kw.get("dt", -0.1), None)
+    for kw, msg in [(dict(L=0), "L must"), (dict(C=6), "multiple of 4"), (dict(C=0), "multiple of 4"),
+                    (dict(n=-1), "n_kept"), (dict(n=1001), "n_kept"), (dict(vt=7), "dtype"),
+                    (dict(dt=float("inf")), "finite"), (dict(z=None), "z is NULL"),
+                    (dict(z=MISALIGNED), "aligned"), (dict(kept=None), "kept_idx is NULL"),
+                    (dict(v=ctypes.c_void_p(0x10004), vt=ut.UT_F32), "aligned")]:
+        assert eu(**kw) == ut.UT_ERR_INVALID_ARG, kw
+        assert msg in ut.last_error(), (kw, ut.last_error())
+    assert eu(n=0, z=None, kept=None, v=None) == ut.UT_OK      # nothing to do
+    ws = ut.ut_fg_flow_loss_workspace_size()
+    lo = lambda **kw: lib.ut_fg_flow_loss(
+        kw.get("v", FAKE), kw.get("vt", ut.UT_BF16), kw.get("e", FAKE), kw.get("z0", FAKE),
+        kw.get("xt", ut.UT_F32), kw.get("L", 1000), kw.get("C", 64), kw.get("kept", FAKE), kw.get("n", 10),
+        kw.get("loss", FAKE), kw.get("grad", None), kw.get("ws", FAKE), kw.get("wsb", ws), None)
+    for kw, status, msg in [(dict(xt=5), ut.UT_ERR_INVALID_ARG, "dtype"),
+                            (dict(loss=None), ut.UT_ERR_INVALID_ARG, "loss is NULL"),
+                            (dict(e=None), ut.UT_ERR_INVALID_ARG, "eps is NULL"),
+                            (dict(grad=MISALIGNED), ut.UT_ERR_INVALID_ARG, "aligned"),
+                            (dict(ws=None), ut.UT_ERR_WORKSPACE, "workspace"),
+                            (dict(wsb=ws - 8), ut.UT_ERR_WORKSPACE, "workspace")]:
+        assert lo(**kw) == status, kw
+        assert msg in ut.last_error(), (kw, ut.last_error())
