@@ -22,6 +22,11 @@ Paper sections (arXiv 2609.23169, "UltraTex"):
     matching loss over the gathered foreground target tokens, with the target
     velocity eps - z_tgt of Eq. 1-2) and Eq. 4 (the Euler step applied only
     at the retained positions).
+  * Foreground-aware decoding input: Sec. 3.4, Eq. 9 (the composite latent:
+    denoised foreground at the retained positions, the canonical background
+    latent tile-repeated over the views elsewhere) and the mask construction
+    of Sec. 3.2 (alpha masks brought to the 1/16 token grid and slightly
+    dilated).
   * Top-K block selection: Sec. 3.3, Eq. 6 (compressed scores from
     mean-pooled query and key blocks) and Eq. 7 (row-wise Top-K over the key
     blocks gives the block mask).
@@ -39,6 +44,7 @@ __all__ = [
     "bsattn_fwd", "bsattn_bwd",
     "block_pool", "topk_block_mask",
     "euler_update_fg", "fg_flow_loss",
+    "composite_latent", "token_mask_from_alpha",
 ]
 
 
@@ -307,3 +313,49 @@ def fg_flow_loss(v, eps, z0, kept_idx):
     loss = float((diff * diff).sum() / (n * C)) if n else 0.0
     grad = 2.0 * diff / (n * C) if n else np.zeros((0, C))
     return loss, grad
+
+
+# ---------------------------------------------------------------------------
+# Composite latent (Sec. 3.4, Eq. 9) and token masks (Sec. 3.2)
+# ---------------------------------------------------------------------------
+
+def composite_latent(x_packed, kept_idx, z_bg, L: int) -> np.ndarray:
+    """Eq. 9: z_mix_i = z_fg_i at a retained position i (packed row k for
+    i = kept_idx[k]) and the canonical background latent elsewhere. z_bg holds
+    one view's token grid [P, C]; tile-repeating it over the views gives
+    position i the background row i mod P. Returns [L, C] in z_bg's dtype
+    (a copy: no arithmetic)."""
+    xp, bg = np.asarray(x_packed), np.asarray(z_bg)
+    P = bg.shape[0]
+    out = np.empty((L,) + bg.shape[1:], dtype=bg.dtype)
+    kept = {int(i): k for k, i in enumerate(np.asarray(kept_idx).tolist())}
+    for i in range(L):
+        out[i] = xp[kept[i]] if i in kept else bg[i % P]
+    return out
+
+
+def token_mask_from_alpha(alpha, patch: int, radius: int, threshold: int = 0) -> np.ndarray:
+    """Sec. 3.2: per-view alpha masks brought to the token grid and dilated.
+
+    Readings (the paper names neither rule): a token is foreground when any
+    pixel of its patch x patch block has alpha > threshold, and the dilation
+    is a (2 radius + 1)^2 square, clipped at the view border.
+    alpha [V, H, W] with H, W multiples of patch -> uint8 [V, H/patch, W/patch].
+    """
+    a = np.asarray(alpha)
+    V, Hp, Wp = a.shape
+    gh, gw = Hp // patch, Wp // patch
+    pooled = np.zeros((V, gh, gw), dtype=bool)
+    for v in range(V):
+        for y in range(gh):
+            for x in range(gw):
+                blk = a[v, y * patch:(y + 1) * patch, x * patch:(x + 1) * patch]
+                pooled[v, y, x] = bool((blk > threshold).any())
+    out = np.zeros((V, gh, gw), dtype=np.uint8)
+    for v in range(V):
+        for y in range(gh):
+            for x in range(gw):
+                y0, y1 = max(0, y - radius), min(gh, y + radius + 1)
+                x0, x1 = max(0, x - radius), min(gw, x + radius + 1)
+                out[v, y, x] = 1 if pooled[v, y0:y1, x0:x1].any() else 0
+    return out

@@ -517,3 +517,58 @@ def test_fg_loss_matches_mse_and_finite_differences():
     eps2 = eps.copy()
     eps2[np.setdiff1d(np.arange(L), kept)] = np.nan
     assert oracle.fg_flow_loss(v, eps2, z0, kept)[0] == loss
+
+
+# ---------------------------------------------------------------------------
+# Composite latent (Sec. 3.4, Eq. 9) and token masks (Sec. 3.2)
+# ---------------------------------------------------------------------------
+
+def test_composite_hand_example():
+    # two views of P = 3 tokens, C = 2; retained positions 1, 3, 5
+    bg = np.array([[10, 11], [12, 13], [14, 15]], dtype=np.float32)
+    packed = np.array([[1, 2], [3, 4], [5, 6]], dtype=np.float32)
+    out = oracle.composite_latent(packed, np.array([1, 3, 5]), bg, 6)
+    assert np.array_equal(out, [[10, 11], [1, 2], [14, 15], [3, 4], [12, 13], [5, 6]])
+
+
+def test_composite_matches_tile_then_index_put():
+    rng = np.random.default_rng(8)
+    V, P, C = 6, 64, 16
+    L = V * P
+    bg = rng.standard_normal((P, C)).astype(np.float32)
+    kept = np.flatnonzero(rng.random(L) < 0.35)
+    packed = rng.standard_normal((kept.size, C)).astype(np.float32)
+    ref = torch.from_numpy(bg).repeat(V, 1)
+    ref[torch.from_numpy(kept)] = torch.from_numpy(packed)
+    out = oracle.composite_latent(packed, kept, bg, L)
+    assert np.array_equal(out, ref.numpy())
+    # nothing kept -> the tiled background; everything kept -> the packed rows
+    assert np.array_equal(oracle.composite_latent(packed[:0], kept[:0], bg, L), np.tile(bg, (V, 1)))
+    full = rng.standard_normal((L, C)).astype(np.float32)
+    assert np.array_equal(oracle.composite_latent(full, np.arange(L), bg, L), full)
+
+
+def test_token_mask_hand_example():
+    # one 64 x 64 view, patch 16 -> 4 x 4 tokens; one bright pixel in token (1, 2)
+    a = np.zeros((1, 64, 64), dtype=np.uint8)
+    a[0, 16 + 5, 32 + 15] = 200
+    m0 = oracle.token_mask_from_alpha(a, 16, 0)
+    assert m0.sum() == 1 and m0[0, 1, 2] == 1
+    m1 = oracle.token_mask_from_alpha(a, 16, 1)
+    assert np.array_equal(m1[0], [[0, 1, 1, 1], [0, 1, 1, 1], [0, 1, 1, 1], [0, 0, 0, 0]])
+    # threshold: a pixel at exactly the threshold is background
+    assert oracle.token_mask_from_alpha(a, 16, 1, threshold=200).sum() == 0
+    assert oracle.token_mask_from_alpha(a, 16, 1, threshold=199).sum() == 9
+
+
+def test_token_mask_matches_reshape_max_and_scipy_dilation():
+    from scipy import ndimage
+    rng = np.random.default_rng(9)
+    V, H, W, patch = 3, 96, 128, 16
+    a = (rng.random((V, H, W)) < 0.002).astype(np.uint8) * rng.integers(1, 256, (V, H, W)).astype(np.uint8)
+    for radius in (0, 1, 2):
+        got = oracle.token_mask_from_alpha(a, patch, radius)
+        pooled = a.reshape(V, H // patch, patch, W // patch, patch).max(axis=(2, 4)) > 0
+        ref = np.stack([ndimage.binary_dilation(pooled[v], structure=np.ones((2 * radius + 1,) * 2))
+                        if radius else pooled[v] for v in range(V)]).astype(np.uint8)
+        assert np.array_equal(got, ref), radius
