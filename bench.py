@@ -169,6 +169,52 @@ def time_fg_step(ut, fg_mask, grid: int, dev, stream, C: int = 64, reps: int = 2
     return out
 
 
+def _time(run, stream, reps: int = 20) -> float:
+    import torch
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record(stream)
+    for _ in range(reps):
+        run()
+    e1.record(stream)
+    torch.cuda.synchronize()
+    return e0.elapsed_time(e1) / reps
+
+
+def time_decode_prep(ut, fg_mask, grid: int, dev, stream, C: int = 64) -> dict:
+    """Composite latent of Eq. 9 on the six target views (fp32, 64 channels,
+    background tiled from one view's grid) and the alpha -> token-mask step of
+    Sec. 3.2 on seven 16x-upsampled 2048 x 2048 alpha masks; timed on their
+    own, outside the step."""
+    import numpy as np
+    import torch
+    P = grid * grid
+    L = 6 * P
+    kept = np.flatnonzero(fg_mask[:L])
+    inv = np.full(L, -1, dtype=np.int32)
+    inv[kept] = np.arange(kept.size, dtype=np.int32)
+    inv_d = torch.from_numpy(inv).to(dev)
+    g = torch.Generator(device=dev).manual_seed(6)
+    packed = torch.randn((kept.size, C), device=dev, generator=g)
+    bg = torch.randn((P, C), device=dev, generator=g)
+    mix = torch.empty((L, C), device=dev)
+    views = np.concatenate([fg_mask[:L].reshape(6, grid, grid), fg_mask[-P:].reshape(1, grid, grid)])
+    alpha = torch.from_numpy(np.repeat(np.repeat(views * 255, 16, axis=1), 16, axis=2).astype(np.uint8)).to(dev)
+    tmask = torch.empty((7, grid, grid), dtype=torch.uint8, device=dev)
+    ws = torch.empty(ut.ut_token_mask_workspace_size(7, 16 * grid, 16 * grid, 16), dtype=torch.uint8, device=dev)
+    out = {}
+    for name, run, nbytes in (
+            ("composite", lambda: ut.ut_composite_latent(packed, kept.size, inv_d, bg, mix),
+             L * C * 4 + kept.size * C * 4 + (L - kept.size) * C * 4 + 4 * L),
+            ("token_mask", lambda: ut.ut_token_mask_from_alpha(alpha, 16, 0, 1, tmask, ws),
+             alpha.numel() + 3 * tmask.numel())):
+        st = run()
+        if st != ut.UT_OK:
+            raise ut.UltraTexError(name, st, ut.last_error())
+        ms = _time(run, stream)
+        out[name] = {"ms": round(ms, 4), "bytes": int(nbytes), "gbs": round(nbytes / (ms * 1e-3) / 1e9, 1)}
+    return out
+
+
 def main():
     args = parse()
     if args.gpus != 1:
@@ -304,6 +350,7 @@ def main():
     }
     result["topk_mask"] = time_topk(ut, q, k, blk, W.kept_off_diagonal(wl.rho, nb), stream)
     result["fg_step"] = time_fg_step(ut, inst.fg_mask, wl.grid, dev, stream)
+    result["decode_prep"] = time_decode_prep(ut, inst.fg_mask, wl.grid, dev, stream)
     if not args.no_cpu_baseline:
         result["cpu_baseline"] = cpu_baseline(inst, args.cpu_seconds)
     print(json.dumps(result), flush=True)

@@ -270,6 +270,51 @@ ut_status ut_fg_flow_loss(const void* v, ut_dtype v_dtype, const void* eps, cons
                           float* grad, void* workspace, size_t workspace_bytes,
                           hipStream_t stream);
 
+/* ------------------------------------------------------------------------
+ * Composite latent for foreground-aware decoding (Sec. 3.4, Eq. 9): row i of
+ * z_mix is the denoised packed row inv_idx[i] where position i was retained,
+ * and otherwise row i mod bg_rows of the canonical background latent z_bg
+ * (one view's token grid, tile-repeated over the views).
+ *
+ * x_packed  [n_kept, row_bytes] packed rows (NULL allowed when n_kept = 0).
+ * inv_idx   [L] int32, the inverse map of ut_drop_background: the packed
+ *           index of each position, -1 where dropped. Entries outside
+ *           [0, n_kept) take the background row.
+ * z_bg      [bg_rows, row_bytes]. z_mix: [L, row_bytes] output (every row
+ *           written). row_bytes: a positive multiple of 16; the row buffers
+ *           16-byte aligned. A byte copy: any element type.
+ * Errors: L < 1 or >= 2^31, bg_rows < 1, n_kept < 0 or > L, row_bytes not
+ *         a positive multiple of 16, null or misaligned pointers ->
+ *         UT_ERR_INVALID_ARG.
+ * ---------------------------------------------------------------------- */
+ut_status ut_composite_latent(const void* x_packed, int64_t n_kept,
+                              const int32_t* inv_idx, int64_t L, const void* z_bg,
+                              int64_t bg_rows, int64_t row_bytes, void* z_mix,
+                              hipStream_t stream);
+
+/* ------------------------------------------------------------------------
+ * Token-grid foreground masks from alpha masks (Sec. 3.2, "Mask Construction
+ * and Sequence Compression"): a token is foreground when any pixel of its
+ * patch x patch block has alpha > threshold; the result is then dilated by a
+ * (2 radius + 1)^2 square, clipped at each view's border. (The paper gives
+ * neither rule; these are the readings taken.)
+ *
+ * alpha       uint8 [V, Hp, Wp], 16-byte aligned; Hp and Wp multiples of
+ *             patch; patch a positive multiple of 16 (16 in the paper: the
+ *             latent token grid is 1/16 of the image).
+ * threshold   0..255. radius: 0..16 (0 = no dilation).
+ * token_mask  uint8 [V, Hp / patch, Wp / patch] output, 1 = foreground.
+ * workspace   ut_token_mask_workspace_size bytes (the undilated mask),
+ *             unused (may be NULL) when radius = 0.
+ * Errors: bad sizes, patch, threshold or radius, null or misaligned pointers
+ *         -> UT_ERR_INVALID_ARG; workspace too small -> UT_ERR_WORKSPACE.
+ * ---------------------------------------------------------------------- */
+size_t ut_token_mask_workspace_size(int32_t V, int32_t Hp, int32_t Wp, int32_t patch);
+ut_status ut_token_mask_from_alpha(const uint8_t* alpha, int32_t V, int32_t Hp,
+                                   int32_t Wp, int32_t patch, int32_t threshold,
+                                   int32_t radius, uint8_t* token_mask, void* workspace,
+                                   size_t workspace_bytes, hipStream_t stream);
+
 #ifdef __cplusplus
 }
 #endif

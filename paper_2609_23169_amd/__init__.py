@@ -34,6 +34,7 @@ EXPORTS = [
     "ut_bsattn_fwd", "ut_bsattn_bwd_workspace_size", "ut_bsattn_bwd",
     "ut_topk_block_mask_workspace_size", "ut_topk_block_mask",
     "ut_euler_update_foreground", "ut_fg_flow_loss_workspace_size", "ut_fg_flow_loss",
+    "ut_composite_latent", "ut_token_mask_workspace_size", "ut_token_mask_from_alpha",
 ]
 
 
@@ -60,6 +61,9 @@ _SIGS = {
     "ut_topk_block_mask": (_c.c_int, [_vp, _vp, _i32, _i32, _i32, _i32, _i32, _i32, _vp, _vp, _sz, _vp]),
     "ut_euler_update_foreground": (_c.c_int, [_vp, _i64, _i64, _vp, _c.c_int, _vp, _i64, _f32, _vp]),
     "ut_fg_flow_loss_workspace_size": (_sz, []),
+    "ut_composite_latent": (_c.c_int, [_vp, _i64, _vp, _i64, _vp, _i64, _i64, _vp, _vp]),
+    "ut_token_mask_workspace_size": (_sz, [_i32, _i32, _i32, _i32]),
+    "ut_token_mask_from_alpha": (_c.c_int, [_vp, _i32, _i32, _i32, _i32, _i32, _i32, _vp, _vp, _sz, _vp]),
     "ut_fg_flow_loss": (_c.c_int, [_vp, _c.c_int, _vp, _vp, _c.c_int, _i64, _i64, _vp, _i64, _vp, _vp,
                                    _vp, _sz, _vp]),
 }
@@ -266,6 +270,32 @@ def ut_fg_flow_loss(v, eps, z0, kept_idx, n_kept: int, loss, grad, workspace, st
                                  _p(workspace), ws_bytes, _stream(stream))
 
 
+def ut_composite_latent(x_packed, n_kept: int, inv_idx, z_bg, z_mix, stream=None) -> int:
+    _need(z_mix.dim() >= 1 and inv_idx.dtype == torch.int32 and inv_idx.numel() == z_mix.shape[0],
+          "inv_idx: int32 [L], z_mix: [L, ...]")
+    L = z_mix.shape[0]
+    row_bytes = _nbytes(z_mix) // L
+    _need(z_bg.dtype == z_mix.dtype and _nbytes(z_bg) % row_bytes == 0, "z_bg: [P, ...] rows like z_mix")
+    _need(x_packed.dtype == z_mix.dtype and _nbytes(x_packed) >= n_kept * row_bytes, "x_packed rows")
+    return lib().ut_composite_latent(_p(x_packed) if n_kept else None, n_kept, _p(inv_idx), L, _p(z_bg),
+                                     _nbytes(z_bg) // row_bytes, row_bytes, _p(z_mix), _stream(stream))
+
+
+def ut_token_mask_workspace_size(V: int, Hp: int, Wp: int, patch: int) -> int:
+    return int(lib().ut_token_mask_workspace_size(V, Hp, Wp, patch))
+
+
+def ut_token_mask_from_alpha(alpha, patch: int, threshold: int, radius: int, token_mask, workspace,
+                             stream=None) -> int:
+    _need(alpha.dtype == torch.uint8 and alpha.dim() == 3, "alpha: uint8 [V, Hp, Wp]")
+    V, Hp, Wp = alpha.shape
+    _need(token_mask.dtype == torch.uint8 and token_mask.numel() >= V * (Hp // patch) * (Wp // patch),
+          "token_mask: uint8 [V, Hp/patch, Wp/patch]")
+    ws_bytes = _nbytes(workspace) if workspace is not None else 0
+    return lib().ut_token_mask_from_alpha(_p(alpha), V, Hp, Wp, patch, threshold, radius, _p(token_mask),
+                                          _p(workspace), ws_bytes, _stream(stream))
+
+
 # ---------------------------------------------------------------------------
 # Allocating helpers (raise on error)
 # ---------------------------------------------------------------------------
@@ -368,3 +398,22 @@ def fg_flow_loss(v, eps, z0, kept_idx, with_grad: bool = True, workspace=None, s
         workspace = torch.empty(ut_fg_flow_loss_workspace_size(), dtype=torch.uint8, device=eps.device)
     _raise("ut_fg_flow_loss", ut_fg_flow_loss(v, eps, z0, kept_idx, n, loss, grad, workspace, stream))
     return loss, grad
+
+
+def composite_latent(x_packed, inv_idx, z_bg, n_kept: int, stream=None):
+    """z_mix [L, ...] of Eq. 9 (packed rows where kept, tiled z_bg elsewhere)."""
+    L = inv_idx.numel()
+    z_mix = torch.empty((L,) + tuple(z_bg.shape[1:]), dtype=z_bg.dtype, device=z_bg.device)
+    _raise("ut_composite_latent", ut_composite_latent(x_packed, n_kept, inv_idx, z_bg, z_mix, stream))
+    return z_mix
+
+
+def token_mask_from_alpha(alpha, patch: int = 16, threshold: int = 0, radius: int = 1, stream=None):
+    """uint8 [V, Hp/patch, Wp/patch] token-grid foreground masks."""
+    V, Hp, Wp = alpha.shape
+    out = torch.empty((V, Hp // patch, Wp // patch), dtype=torch.uint8, device=alpha.device)
+    ws = torch.empty(max(ut_token_mask_workspace_size(V, Hp, Wp, patch), 1), dtype=torch.uint8,
+                     device=alpha.device)
+    _raise("ut_token_mask_from_alpha", ut_token_mask_from_alpha(alpha, patch, threshold, radius, out, ws,
+                                                                stream))
+    return out

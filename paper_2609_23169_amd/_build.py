@@ -18,7 +18,7 @@ OBJ = os.path.join(HERE, "_build")
 
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 SOURCES = ["api.cpp", "btd.hip", "block_index.hip", "bsattn_fwd.hip", "bsattn_bwd.hip",
-           "topk_mask.hip", "fg_step.hip"]
+           "topk_mask.hip", "fg_step.hip", "composite.hip"]
 FLAGS = [
     "--offload-arch=gfx950", "-O3", "-std=c++17", "-fPIC",
     "-Wall", "-Wno-unused-function",

@@ -324,4 +324,63 @@ ut_status ut_fg_flow_loss(const void* v, ut_dtype v_dtype, const void* eps, cons
                    "loss launch");
 }
 
+ut_status ut_composite_latent(const void* x_packed, int64_t n_kept, const int32_t* inv_idx,
+                              int64_t L, const void* z_bg, int64_t bg_rows, int64_t row_bytes,
+                              void* z_mix, hipStream_t stream) {
+  static const char* fn = "ut_composite_latent";
+  g_last_error[0] = 0;
+  if (L < 1 || L >= ((int64_t)1 << 31))
+    return fail(UT_ERR_INVALID_ARG, "%s: L must be in [1, 2^31) (got %lld)", fn, (long long)L);
+  if (bg_rows < 1)
+    return fail(UT_ERR_INVALID_ARG, "%s: bg_rows must be >= 1 (got %lld)", fn, (long long)bg_rows);
+  if (n_kept < 0 || n_kept > L)
+    return fail(UT_ERR_INVALID_ARG, "%s: n_kept must be in [0, L] (got %lld)", fn, (long long)n_kept);
+  if (row_bytes <= 0 || row_bytes % 16 != 0)
+    return fail(UT_ERR_INVALID_ARG, "%s: row_bytes must be a positive multiple of 16 (got %lld)",
+                fn, (long long)row_bytes);
+  if (n_kept > 0) UT_TRY(check_ptr(fn, "x_packed", x_packed, 16));
+  UT_TRY(check_ptr(fn, "inv_idx", inv_idx, 4));
+  UT_TRY(check_ptr(fn, "z_bg", z_bg, 16));
+  UT_TRY(check_ptr(fn, "z_mix", z_mix, 16));
+  return check_hip(launch_composite(x_packed, n_kept, inv_idx, L, z_bg, bg_rows, row_bytes, z_mix,
+                                    stream),
+                   "composite launch");
+}
+
+size_t ut_token_mask_workspace_size(int32_t V, int32_t Hp, int32_t Wp, int32_t patch) {
+  if (V < 1 || Hp < 1 || Wp < 1 || patch < 1) return 0;
+  return (size_t)V * (Hp / patch) * (Wp / patch);
+}
+
+ut_status ut_token_mask_from_alpha(const uint8_t* alpha, int32_t V, int32_t Hp, int32_t Wp,
+                                   int32_t patch, int32_t threshold, int32_t radius,
+                                   uint8_t* token_mask, void* workspace, size_t workspace_bytes,
+                                   hipStream_t stream) {
+  static const char* fn = "ut_token_mask_from_alpha";
+  g_last_error[0] = 0;
+  if (V < 1 || Hp < 1 || Wp < 1)
+    return fail(UT_ERR_INVALID_ARG, "%s: V, Hp, Wp must be >= 1", fn);
+  if (patch < 16 || patch % 16 != 0 || Hp % patch != 0 || Wp % patch != 0)
+    return fail(UT_ERR_INVALID_ARG,
+                "%s: patch must be a positive multiple of 16 dividing Hp and Wp (got %d for %d x %d)",
+                fn, patch, Hp, Wp);
+  if (threshold < 0 || threshold > 255)
+    return fail(UT_ERR_INVALID_ARG, "%s: threshold must be in [0, 255] (got %d)", fn, threshold);
+  if (radius < 0 || radius > 16)
+    return fail(UT_ERR_INVALID_ARG, "%s: radius must be in [0, 16] (got %d)", fn, radius);
+  if ((int64_t)V * Hp * Wp >= ((int64_t)1 << 40))
+    return fail(UT_ERR_INVALID_ARG, "%s: alpha too large", fn);
+  UT_TRY(check_ptr(fn, "alpha", alpha, 16));
+  UT_TRY(check_ptr(fn, "token_mask", token_mask, 1));
+  if (radius > 0) {
+    const size_t need = ut_token_mask_workspace_size(V, Hp, Wp, patch);
+    if (!workspace || workspace_bytes < need)
+      return fail(UT_ERR_WORKSPACE, "%s: workspace of %zu bytes required (got %zu)", fn, need,
+                  workspace ? workspace_bytes : (size_t)0);
+  }
+  return check_hip(launch_token_mask(alpha, V, Hp, Wp, patch, threshold, radius, token_mask,
+                                     static_cast<uint8_t*>(workspace), stream),
+                   "token mask launch");
+}
+
 }  // extern "C"

@@ -59,4 +59,11 @@ hipError_t launch_fg_loss(const void* v, bool v_bf16, const void* eps, const voi
                           bool x_bf16, int64_t L, int64_t C, const int32_t* kept, int64_t n,
                           float* loss, float* grad, double* partial, hipStream_t s);
 
+// ---- Composite latent and token masks (composite.hip) ----
+hipError_t launch_composite(const void* packed, int64_t n_kept, const int32_t* inv, int64_t L,
+                            const void* bg, int64_t bg_rows, int64_t row_bytes, void* out,
+                            hipStream_t s);
+hipError_t launch_token_mask(const uint8_t* alpha, int V, int Hp, int Wp, int patch, int thr,
+                             int radius, uint8_t* out, uint8_t* pooled, hipStream_t s);
+
 }  // namespace ut

@@ -168,3 +168,28 @@ def test_foreground_step_calls_reject_bad_arguments():
                             (dict(wsb=ws - 8), ut.UT_ERR_WORKSPACE, "workspace")]:
         assert lo(**kw) == status, kw
         assert msg in ut.last_error(), (kw, ut.last_error())
+
+
+def test_composite_and_token_mask_reject_bad_arguments():
+    lib = ut.lib()
+    co = lambda **kw: lib.ut_composite_latent(
+        kw.get("xp", FAKE), kw.get("n", 10), kw.get("inv", FAKE), kw.get("L", 100), kw.get("bg", FAKE),
+        kw.get("P", 16), kw.get("rb", 256), kw.get("out", FAKE), None)
+    for kw, msg in [(dict(L=0), "L must"), (dict(P=0), "bg_rows"), (dict(n=101), "n_kept"),
+                    (dict(rb=100), "multiple of 16"), (dict(xp=None), "x_packed is NULL"),
+                    (dict(inv=None), "inv_idx is NULL"), (dict(out=MISALIGNED), "aligned")]:
+        assert co(**kw) == ut.UT_ERR_INVALID_ARG, kw
+        assert msg in ut.last_error(), (kw, ut.last_error())
+    assert ut.ut_token_mask_workspace_size(7, 2048, 2048, 16) == 7 * 128 * 128
+    tm = lambda **kw: lib.ut_token_mask_from_alpha(
+        kw.get("a", FAKE), kw.get("V", 2), kw.get("H", 64), kw.get("W", 96), kw.get("p", 16),
+        kw.get("t", 0), kw.get("r", 1), kw.get("m", FAKE), kw.get("ws", FAKE), kw.get("wsb", 2 * 4 * 6), None)
+    for kw, status, msg in [(dict(p=8), ut.UT_ERR_INVALID_ARG, "patch"),
+                            (dict(W=100), ut.UT_ERR_INVALID_ARG, "patch"),
+                            (dict(t=256), ut.UT_ERR_INVALID_ARG, "threshold"),
+                            (dict(r=-1), ut.UT_ERR_INVALID_ARG, "radius"),
+                            (dict(a=MISALIGNED), ut.UT_ERR_INVALID_ARG, "aligned"),
+                            (dict(m=None), ut.UT_ERR_INVALID_ARG, "token_mask is NULL"),
+                            (dict(wsb=47), ut.UT_ERR_WORKSPACE, "workspace")]:
+        assert tm(**kw) == status, kw
+        assert msg in ut.last_error(), (kw, ut.last_error())
