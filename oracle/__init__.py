@@ -253,7 +253,7 @@ def block_pool(x, block: int) -> np.ndarray:
     return out
 
 
-def topk_block_mask(q, k, block: int, k_keep: int):
+def topk_block_mask(q, k, block: int, k_keep: int, prefix_blocks: int = 0):
     """Eq. 6-7: per (b, h), S_c = pool(Q) pool(K)^T and M_c[i, j] = 1 for the
     k_keep largest entries of row i of S_c.
 
@@ -261,19 +261,28 @@ def topk_block_mask(q, k, block: int, k_keep: int):
     count as k_keep (k_keep >= N_k keeps every block); equal scores are ranked
     lower j first (the paper does not order ties); no block is forced, the
     diagonal included. A stable sort of the negated row is the selection step.
+    prefix_blocks = P > 0 models the always-kept text tokens at the head of
+    the joint sequence (512 in the paper's token counts): the first P key
+    blocks are kept for every row, the first P query blocks keep every block,
+    and the k_keep best blocks are chosen among j >= P.
     Returns (mask uint8 [B, H, Nq, Nk], S_c float64 [B, H, Nq, Nk]).
     """
     PQ, PK = block_pool(q, block), block_pool(k, block)
     B, H, nq, _ = PQ.shape
     nk = PK.shape[2]
+    P = min(prefix_blocks, nk)
     Sc = np.zeros((B, H, nq, nk))
     mask = np.zeros((B, H, nq, nk), dtype=np.uint8)
     for b in range(B):
         for h in range(H):
             Sc[b, h] = PQ[b, h] @ PK[b, h].T
             for i in range(nq):
-                order = np.argsort(-Sc[b, h, i], kind="stable")
-                mask[b, h, i, order[:min(k_keep, nk)]] = 1
+                if i < P:
+                    mask[b, h, i, :] = 1
+                    continue
+                mask[b, h, i, :P] = 1
+                order = P + np.argsort(-Sc[b, h, i, P:], kind="stable")
+                mask[b, h, i, order[:min(k_keep, nk - P)]] = 1
     return mask, Sc
 
 

@@ -572,3 +572,26 @@ def test_token_mask_matches_reshape_max_and_scipy_dilation():
         ref = np.stack([ndimage.binary_dilation(pooled[v], structure=np.ones((2 * radius + 1,) * 2))
                         if radius else pooled[v] for v in range(V)]).astype(np.uint8)
         assert np.array_equal(got, ref), radius
+
+
+def test_topk_dense_prefix_blocks():
+    """Text-prefix reading: prefix columns and rows are dense, the Top-K runs
+    over the remaining key blocks (checked against the no-prefix selection
+    restricted to j >= P, and by brute-force rank)."""
+    rng = np.random.default_rng(12)
+    q = rng.standard_normal((1, 700, 2, 8))
+    k = rng.standard_normal((1, 700, 2, 8))
+    block, P, kk = 64, 3, 4
+    mask, sc = oracle.topk_block_mask(q, k, block, kk, prefix_blocks=P)
+    nb = mask.shape[-1]
+    assert mask[:, :, :P, :].all() and mask[:, :, :, :P].all()
+    assert np.all(mask[:, :, P:, :].sum(-1) == P + kk)
+    for h in range(2):
+        for i in range(P, nb):
+            row = sc[0, h, i]
+            for j in range(P, nb):
+                beaten = sum(1 for jj in range(P, nb) if row[jj] > row[j] or (row[jj] == row[j] and jj < j))
+                assert mask[0, h, i, j] == (1 if beaten < kk else 0)
+    # P = 0 is the plain selection; a prefix covering everything keeps all
+    assert np.array_equal(oracle.topk_block_mask(q, k, block, kk, 0)[0], oracle.topk_block_mask(q, k, block, kk)[0])
+    assert oracle.topk_block_mask(q, k, block, kk, nb)[0].all()
