@@ -114,7 +114,7 @@ def time_topk(ut, q, k, blk: int, k_keep: int, stream, reps: int = 10) -> dict:
     mask = torch.empty((B, H, nb, nb), dtype=torch.uint8, device=q.device)
     ws = torch.empty(ut.ut_topk_block_mask_workspace_size(B, N, H, D, blk), dtype=torch.uint8,
                      device=q.device)
-    run = lambda: ut.ut_topk_block_mask(q, k, blk, k_keep, mask, ws)
+    run = lambda: ut.ut_topk_block_mask(q, k, blk, k_keep, mask, ws)   # no text prefix
     for _ in range(2):
         st = run()
         if st != ut.UT_OK:

@@ -204,6 +204,10 @@ ut_status ut_bsattn_bwd(const void* q, const void* k, const void* v,
  * D           a multiple of 8, at most 512. block: >= 1.
  * k_keep      blocks kept per row, >= 1 (floor(rho N_k) in the paper; the
  *             caller computes it); k_keep >= Nk keeps every block.
+ * prefix_blocks  P in [0, Nk]: leading blocks of always-kept tokens (the
+ *             text tokens of the joint sequence, 512 in the paper's token
+ *             counts): rows i < P keep every block, every row keeps blocks
+ *             j < P, and the k_keep best blocks are chosen among j >= P.
  * block_mask  uint8 [B, H, Nk, Nk] output, Nk = ceil(N / block); 1 = kept.
  * workspace   device scratch of ut_topk_block_mask_workspace_size bytes
  *             (the pooled rows, fp32), 16-byte aligned.
@@ -212,7 +216,8 @@ ut_status ut_bsattn_bwd(const void* q, const void* k, const void* v,
  * arithmetic may differ from an exact-arithmetic selection, and is then still
  * a valid Top-K of the fp32 scores. Inputs must be finite.
  * Errors: sizes < 1, D not a multiple of 8 or > 512, B > 65535, null or
- *         misaligned pointers, k_keep < 1 -> UT_ERR_INVALID_ARG; a row of
+ *         misaligned pointers, k_keep < 1, prefix_blocks outside [0, Nk] ->
+ *         UT_ERR_INVALID_ARG; a row of
  *         scores too long for one workgroup's LDS (Nk + D > 16384) ->
  *         UT_ERR_UNSUPPORTED; workspace too small -> UT_ERR_WORKSPACE.
  * ---------------------------------------------------------------------- */
@@ -220,7 +225,7 @@ size_t ut_topk_block_mask_workspace_size(int32_t B, int32_t N, int32_t H, int32_
                                          int32_t block);
 ut_status ut_topk_block_mask(const void* q, const void* k, int32_t B, int32_t N,
                              int32_t H, int32_t D, int32_t block, int32_t k_keep,
-                             uint8_t* block_mask, void* workspace,
+                             int32_t prefix_blocks, uint8_t* block_mask, void* workspace,
                              size_t workspace_bytes, hipStream_t stream);
 
 /* ------------------------------------------------------------------------

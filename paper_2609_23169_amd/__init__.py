@@ -58,7 +58,8 @@ _SIGS = {
     "ut_bsattn_bwd": (_c.c_int, [_vp, _vp, _vp, _vp, _vp, _vp, _vp, _vp, _vp, _i32, _i32, _i32, _i32, _i32,
                                  _vp, _vp, _vp, _vp, _f32, _vp, _sz, _vp]),
     "ut_topk_block_mask_workspace_size": (_sz, [_i32, _i32, _i32, _i32, _i32]),
-    "ut_topk_block_mask": (_c.c_int, [_vp, _vp, _i32, _i32, _i32, _i32, _i32, _i32, _vp, _vp, _sz, _vp]),
+    "ut_topk_block_mask": (_c.c_int, [_vp, _vp, _i32, _i32, _i32, _i32, _i32, _i32, _i32, _vp, _vp, _sz,
+                                      _vp]),
     "ut_euler_update_foreground": (_c.c_int, [_vp, _i64, _i64, _vp, _c.c_int, _vp, _i64, _f32, _vp]),
     "ut_fg_flow_loss_workspace_size": (_sz, []),
     "ut_composite_latent": (_c.c_int, [_vp, _i64, _vp, _i64, _vp, _i64, _i64, _vp, _vp]),
@@ -224,7 +225,8 @@ def ut_topk_block_mask_workspace_size(B: int, N: int, H: int, D: int, block: int
     return int(lib().ut_topk_block_mask_workspace_size(B, N, H, D, block))
 
 
-def ut_topk_block_mask(q, k, block: int, k_keep: int, block_mask, workspace, stream=None) -> int:
+def ut_topk_block_mask(q, k, block: int, k_keep: int, block_mask, workspace, prefix_blocks: int = 0,
+                       stream=None) -> int:
     _need(q.dim() == 4 and k.shape == q.shape, "q, k: [B, N, H, D], same shape")
     _need(q.dtype == torch.bfloat16 and k.dtype == torch.bfloat16, "q, k: bf16")
     B, N, H, D = q.shape
@@ -232,8 +234,8 @@ def ut_topk_block_mask(q, k, block: int, k_keep: int, block_mask, workspace, str
     _need(block_mask.dtype == torch.uint8 and block_mask.numel() >= B * H * nb * nb,
           "block_mask: uint8 [B, H, Nk, Nk]")
     ws_bytes = _nbytes(workspace) if workspace is not None else 0
-    return lib().ut_topk_block_mask(_p(q), _p(k), B, N, H, D, block, k_keep, _p(block_mask),
-                                    _p(workspace), ws_bytes, _stream(stream))
+    return lib().ut_topk_block_mask(_p(q), _p(k), B, N, H, D, block, k_keep, prefix_blocks,
+                                    _p(block_mask), _p(workspace), ws_bytes, _stream(stream))
 
 
 def _dtype_code(t) -> int:
@@ -370,15 +372,17 @@ def bsattn_bwd(q, k, v, o, dout, lse, index, block: int, softmax_scale: float, w
     return dq, dk, dv
 
 
-def topk_block_mask(q, k, block: int, k_keep: int, workspace=None, stream=None):
-    """Block mask [B, H, Nk, Nk] uint8 of the k_keep best key blocks per query block."""
+def topk_block_mask(q, k, block: int, k_keep: int, prefix_blocks: int = 0, workspace=None, stream=None):
+    """Block mask [B, H, Nk, Nk] uint8 of the k_keep best key blocks per query
+    block (plus the dense leading prefix blocks, if any)."""
     B, N, H, D = q.shape
     nb = -(-N // block)
     mask = torch.empty((B, H, nb, nb), dtype=torch.uint8, device=q.device)
     if workspace is None:
         workspace = torch.empty(max(ut_topk_block_mask_workspace_size(B, N, H, D, block), 16),
                                 dtype=torch.uint8, device=q.device)
-    _raise("ut_topk_block_mask", ut_topk_block_mask(q, k, block, k_keep, mask, workspace, stream))
+    _raise("ut_topk_block_mask", ut_topk_block_mask(q, k, block, k_keep, mask, workspace, prefix_blocks,
+                                                    stream))
     return mask
 
 

@@ -232,8 +232,9 @@ size_t ut_topk_block_mask_workspace_size(int32_t B, int32_t N, int32_t H, int32_
 }
 
 ut_status ut_topk_block_mask(const void* q, const void* k, int32_t B, int32_t N, int32_t H,
-                             int32_t D, int32_t block, int32_t k_keep, uint8_t* block_mask,
-                             void* workspace, size_t workspace_bytes, hipStream_t stream) {
+                             int32_t D, int32_t block, int32_t k_keep, int32_t prefix_blocks,
+                             uint8_t* block_mask, void* workspace, size_t workspace_bytes,
+                             hipStream_t stream) {
   static const char* fn = "ut_topk_block_mask";
   g_last_error[0] = 0;
   if (B < 1 || N < 1 || H < 1 || block < 1)
@@ -247,6 +248,9 @@ ut_status ut_topk_block_mask(const void* q, const void* k, int32_t B, int32_t N,
   const int64_t nblk = ((int64_t)N + block - 1) / block;
   if ((int64_t)B * N * H * D >= (int64_t)1 << 40 || (int64_t)B * H * nblk >= (int64_t)1 << 31)
     return fail(UT_ERR_INVALID_ARG, "%s: problem too large", fn);
+  if (prefix_blocks < 0 || prefix_blocks > nblk)
+    return fail(UT_ERR_INVALID_ARG, "%s: prefix_blocks must be in [0, %lld] (got %d)", fn,
+                (long long)nblk, prefix_blocks);
   if (topk_rows_per_group(D, (int)nblk) == 0)
     return fail(UT_ERR_UNSUPPORTED, "%s: %lld blocks per row do not fit one workgroup", fn,
                 (long long)nblk);
@@ -258,8 +262,8 @@ ut_status ut_topk_block_mask(const void* q, const void* k, int32_t B, int32_t N,
     return fail(UT_ERR_WORKSPACE, "%s: workspace of %zu bytes required (got %zu)", fn, need,
                 workspace ? workspace_bytes : (size_t)0);
   UT_TRY(check_ptr(fn, "workspace", workspace, 16));
-  return check_hip(launch_topk_block_mask(q, k, B, N, H, D, block, k_keep, block_mask,
-                                          static_cast<float*>(workspace), stream),
+  return check_hip(launch_topk_block_mask(q, k, B, N, H, D, block, k_keep, prefix_blocks,
+                                          block_mask, static_cast<float*>(workspace), stream),
                    "top-k launch");
 }
 

@@ -48,7 +48,7 @@ constexpr int64_t kTopkMaxLds = 65536;   // LDS bytes of one selection workgroup
 // Query blocks per selection workgroup (16, 4 or 1), 0 if one row does not fit.
 int topk_rows_per_group(int D, int nblk);
 hipError_t launch_topk_block_mask(const void* q, const void* k, int B, int N, int H, int D,
-                                  int block, int k_keep, uint8_t* mask, float* pooled,
+                                  int block, int k_keep, int prefix, uint8_t* mask, float* pooled,
                                   hipStream_t s);
 
 // ---- Foreground Euler update and loss (fg_step.hip) ----

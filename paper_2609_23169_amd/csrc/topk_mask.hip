@@ -16,7 +16,9 @@
 //            radix select (counts by ballot and scalar popcount) finds the
 //            k-th largest key, and the row of the mask keeps every larger key
 //            plus, of the keys equal to it, the lowest block indices up to k
-//            in total.
+//            in total. With P prefix blocks (always-kept text tokens), the
+//            first P rows are dense, the first P columns are always kept, and
+//            the k best blocks are chosen among the rest.
 #include <algorithm>
 
 #include "common.h"
@@ -108,14 +110,17 @@ struct RowKeys {
 // One wave selects rows r0, r0 + step, ... of the workgroup's score rows in
 // `keys` ([rows][nk] order keys) and writes their mask rows.
 template <int M64>
-__device__ void select_rows(const uint32_t* keys, uint8_t* mask_rows, int rows, int r0, int step,
-                            int nk, int k_keep, int lane) {
+__device__ void select_rows(uint32_t* keys, uint8_t* mask_rows, int i0, int rows, int r0,
+                            int step, int nk, int k_keep, int prefix, int lane) {
   for (int r = r0; r < rows; r += step) {
     uint8_t* mrow = mask_rows + (int64_t)r * nk;
-    if (k_keep >= nk) {
+    if (i0 + r < prefix || k_keep >= nk - prefix) {   // a dense row
       for (int j = lane; j < nk; j += 64) mrow[j] = 1;
       continue;
     }
+    // Prefix columns are always kept: give them key 0, which no threshold
+    // accepts (every score maps to a key >= 1), and choose among the rest.
+    for (int j = lane; j < prefix; j += 64) keys[r * nk + j] = 0u;
     const RowKeys<M64> rk(keys + r * nk, nk, lane);
     // T = the largest key with at least k_keep keys >= T, i.e. the k-th largest.
     uint32_t T = 0;
@@ -130,7 +135,7 @@ __device__ void select_rows(const uint32_t* keys, uint8_t* mask_rows, int rows, 
       const bool tie = j < nk && key == T;
       const uint64_t tm = __ballot(tie);
       const int before = __popcll(tm & ((1ull << lane) - 1ull));
-      if (j < nk) mrow[j] = (key > T || (tie && before < quota)) ? 1 : 0;
+      if (j < nk) mrow[j] = (j < prefix || key > T || (tie && before < quota)) ? 1 : 0;
       quota -= __popcll(tm);
     };
     if constexpr (M64 > 0) {
@@ -156,7 +161,8 @@ template <int D>
 __global__ __launch_bounds__(kSelMfmaThreads) void select_mfma_kernel(const float* __restrict__ pq,
                                                                   const float* __restrict__ pk,
                                                                   uint8_t* __restrict__ mask,
-                                                                  int nq, int nk, int k_keep) {
+                                                                  int nq, int nk, int k_keep,
+                                                                  int prefix) {
   constexpr int QR = 16;
   __shared__ __attribute__((aligned(16))) float sq[QR * D];
   extern __shared__ uint32_t keys[];   // [QR][nk]
@@ -191,8 +197,8 @@ __global__ __launch_bounds__(kSelMfmaThreads) void select_mfma_kernel(const floa
     }
   }
   __syncthreads();
-  select_rows<16>(keys, mask + (bh * nq + i0) * (int64_t)nk, rows, w, kSelMfmaThreads / 64, nk, k_keep,
-                  lane);
+  select_rows<16>(keys, mask + (bh * nq + i0) * (int64_t)nk, i0, rows, w, kSelMfmaThreads / 64, nk,
+                  k_keep, prefix, lane);
 }
 
 // Generic path: QR query blocks per workgroup, any D (multiple of 8).
@@ -200,7 +206,8 @@ template <int QR>
 __global__ __launch_bounds__(kSelThreads) void select_kernel(const float* __restrict__ pq,
                                                              const float* __restrict__ pk,
                                                              uint8_t* __restrict__ mask, int D,
-                                                             int nq, int nk, int k_keep) {
+                                                             int nq, int nk, int k_keep,
+                                                             int prefix) {
   extern __shared__ float smem[];   // [QR][D] pooled query rows, then [QR][nk] keys
   float* const sq = smem;
   uint32_t* const keys = reinterpret_cast<uint32_t*>(smem + QR * D);
@@ -234,27 +241,27 @@ __global__ __launch_bounds__(kSelThreads) void select_kernel(const float* __rest
     for (int r = 0; r < QR; ++r) keys[r * nk + j] = order_key(acc[r] + 0.0f);   // -0 -> +0
   }
   __syncthreads();
-  select_rows<0>(keys, mask + (bh * nq + i0) * (int64_t)nk, rows, threadIdx.x >> 6,
-                 kSelThreads / 64, nk, k_keep, threadIdx.x & 63);
+  select_rows<0>(keys, mask + (bh * nq + i0) * (int64_t)nk, i0, rows, threadIdx.x >> 6,
+                 kSelThreads / 64, nk, k_keep, prefix, threadIdx.x & 63);
 }
 
 template <int QR>
 hipError_t launch_select(const float* pq, const float* pk, uint8_t* mask, int B, int H, int D,
-                         int nq, int k_keep, hipStream_t s) {
+                         int nq, int k_keep, int prefix, hipStream_t s) {
   const int groups = (nq + QR - 1) / QR;
   const size_t lds = (size_t)QR * (D + nq) * sizeof(float);
   hipLaunchKernelGGL((select_kernel<QR>), dim3((unsigned)((int64_t)B * H * groups)),
-                     dim3(kSelThreads), lds, s, pq, pk, mask, D, nq, nq, k_keep);
+                     dim3(kSelThreads), lds, s, pq, pk, mask, D, nq, nq, k_keep, prefix);
   return hipGetLastError();
 }
 
 template <int D>
 hipError_t launch_select_mfma(const float* pq, const float* pk, uint8_t* mask, int B, int H,
-                              int nq, int k_keep, hipStream_t s) {
+                              int nq, int k_keep, int prefix, hipStream_t s) {
   const int groups = (nq + 15) / 16;
   hipLaunchKernelGGL((select_mfma_kernel<D>), dim3((unsigned)((int64_t)B * H * groups)),
                      dim3(kSelMfmaThreads), (size_t)16 * nq * sizeof(uint32_t), s, pq, pk, mask, nq,
-                     nq, k_keep);
+                     nq, k_keep, prefix);
   return hipGetLastError();
 }
 
@@ -268,7 +275,7 @@ int topk_rows_per_group(int D, int nblk) {
 }
 
 hipError_t launch_topk_block_mask(const void* q, const void* k, int B, int N, int H, int D,
-                                  int block, int k_keep, uint8_t* mask, float* pooled,
+                                  int block, int k_keep, int prefix, uint8_t* mask, float* pooled,
                                   hipStream_t s) {
   const int nblk = (N + block - 1) / block;
   float* pq = pooled;
@@ -282,12 +289,12 @@ hipError_t launch_topk_block_mask(const void* q, const void* k, int B, int N, in
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
   if ((D == 64 || D == 128) && 16 * (int64_t)(D + nblk) * 4 <= kTopkMaxLds)
-    return D == 128 ? launch_select_mfma<128>(pq, pk, mask, B, H, nblk, k_keep, s)
-                    : launch_select_mfma<64>(pq, pk, mask, B, H, nblk, k_keep, s);
+    return D == 128 ? launch_select_mfma<128>(pq, pk, mask, B, H, nblk, k_keep, prefix, s)
+                    : launch_select_mfma<64>(pq, pk, mask, B, H, nblk, k_keep, prefix, s);
   const int qr = topk_rows_per_group(D, nblk);
-  if (qr == 16) return launch_select<16>(pq, pk, mask, B, H, D, nblk, k_keep, s);
-  if (qr == 4) return launch_select<4>(pq, pk, mask, B, H, D, nblk, k_keep, s);
-  return launch_select<1>(pq, pk, mask, B, H, D, nblk, k_keep, s);
+  if (qr == 16) return launch_select<16>(pq, pk, mask, B, H, D, nblk, k_keep, prefix, s);
+  if (qr == 4) return launch_select<4>(pq, pk, mask, B, H, D, nblk, k_keep, prefix, s);
+  return launch_select<1>(pq, pk, mask, B, H, D, nblk, k_keep, prefix, s);
 }
 
 }  // namespace ut

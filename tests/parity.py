@@ -96,11 +96,17 @@ def to_np64(t):
     return t.detach().to(torch.float64).cpu().numpy() if isinstance(t, torch.Tensor) else np.asarray(t, np.float64)
 
 
-def check_topk(mask_gpu, ref_mask, scores, tol, k_keep, label=""):
+def check_topk(mask_gpu, ref_mask, scores, tol, k_keep, label="", prefix=0):
     """Every GPU row keeps min(k_keep, Nk) blocks and is a Top-K of the exact
     scores within `tol`; rows whose exact selection is decided by more than
-    the tolerance match the oracle exactly. Returns the decided fraction."""
+    the tolerance match the oracle exactly. With `prefix` dense leading
+    blocks, their rows and columns must be all ones and the rest is checked
+    on the remaining blocks. Returns the decided fraction."""
     m = to_np(mask_gpu).astype(np.uint8) if isinstance(mask_gpu, torch.Tensor) else mask_gpu
+    if prefix:
+        assert m[..., :prefix, :].all() and m[..., :, :prefix].all(), f"{label} prefix not dense"
+        sub = lambda a: a[..., prefix:, prefix:]
+        return check_topk(sub(m), sub(ref_mask), sub(scores), sub(tol), k_keep, label)
     nk = m.shape[-1]
     assert set(np.unique(m)) <= {0, 1}, f"{label} mask values {np.unique(m)}"
     assert np.all(m.sum(-1) == min(k_keep, nk)), f"{label} row counts"

@@ -120,7 +120,7 @@ def test_topk_block_mask_rejects_bad_arguments():
     ws = ut.ut_topk_block_mask_workspace_size(1, 1000, 2, 64, 64)
     call = lambda **kw: lib.ut_topk_block_mask(
         kw.get("q", FAKE), kw.get("k", FAKE), kw.get("B", 1), kw.get("N", 1000), kw.get("H", 2),
-        kw.get("D", 64), kw.get("block", 64), kw.get("kk", 3), kw.get("m", FAKE),
+        kw.get("D", 64), kw.get("block", 64), kw.get("kk", 3), kw.get("P", 0), kw.get("m", FAKE),
         kw.get("ws", FAKE), kw.get("wsb", ws), None)
     for kw, status, msg in [
         (dict(N=0), ut.UT_ERR_INVALID_ARG, ">= 1"),
@@ -128,6 +128,8 @@ def test_topk_block_mask_rejects_bad_arguments():
         (dict(D=60), ut.UT_ERR_INVALID_ARG, "multiple of 8"),
         (dict(D=520), ut.UT_ERR_INVALID_ARG, "multiple of 8"),
         (dict(kk=0), ut.UT_ERR_INVALID_ARG, "k_keep"),
+        (dict(P=-1), ut.UT_ERR_INVALID_ARG, "prefix_blocks"),
+        (dict(P=17), ut.UT_ERR_INVALID_ARG, "prefix_blocks"),
         (dict(B=70000), ut.UT_ERR_INVALID_ARG, "65535"),
         (dict(q=None), ut.UT_ERR_INVALID_ARG, "q is NULL"),
         (dict(k=MISALIGNED), ut.UT_ERR_INVALID_ARG, "aligned"),

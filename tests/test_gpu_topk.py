@@ -24,8 +24,8 @@ def _qk(seed, n, H, D, block):
     return c["q"], c["k"]
 
 
-def _run(q, k, block, kk):
-    m = ut.topk_block_mask(q.to(DEV), k.to(DEV), block, kk)
+def _run(q, k, block, kk, prefix=0):
+    m = ut.topk_block_mask(q.to(DEV), k.to(DEV), block, kk, prefix_blocks=prefix)
     torch.cuda.synchronize()
     return m.cpu().numpy()
 
@@ -113,3 +113,30 @@ def test_topk_mask_drives_attention_end_to_end():
     o, lse = ut.bsattn_fwd(q.to(DEV), k.to(DEV), v.to(DEV), idx, 128, scale)
     O, L = oracle.bsattn_fwd(q, k, v, ref, 128, scale)
     check_out(o, lse, O, L, "e2e")
+
+
+@pytest.mark.parametrize("seed,n,H,D,block,kk,P", [
+    (21, 2000, 2, 128, 128, 3, 4),     # MFMA path
+    (22, 1212, 3, 64, 64, 5, 8),
+    (23, 3000, 2, 96, 64, 6, 2),       # fused multiply-add path
+    (24, 900, 1, 128, 128, 20, 3),     # k_keep beyond the remaining blocks: dense
+])
+def test_topk_dense_text_prefix(seed, n, H, D, block, kk, P):
+    q, k = _qk(seed, n, H, D, block)
+    got = _run(q, k, block, kk, P)
+    ref, sc = oracle.topk_block_mask(q, k, block, kk, prefix_blocks=P)
+    check_topk(got, ref, sc, topk_tolerance(q, k, block), kk, f"prefix {seed}", prefix=P)
+
+
+def test_topk_text_prefix_full_size():
+    """512 text tokens ahead of the 2K workload's 77,060 foreground tokens:
+    four dense leading blocks, k = floor(0.1 N_k) among the rest."""
+    inst = W.make(W.WORKLOADS["c2k_train"].with_rho("0.1"), with_qkv=True)
+    g = torch.Generator().manual_seed(25)
+    txt = lambda: torch.randn((1, 512, 24, 128), generator=g).to(torch.bfloat16)
+    q, k = torch.cat([txt(), inst.q], 1), torch.cat([txt(), inst.k], 1)
+    nb = -(-q.shape[1] // 128)
+    kk = W.kept_off_diagonal("0.1", nb)
+    got = _run(q, k, 128, kk, 4)
+    ref, sc = oracle.topk_block_mask(q, k, 128, kk, prefix_blocks=4)
+    assert check_topk(got, ref, sc, topk_tolerance(q, k, 128), kk, "text prefix", prefix=4) > 0.5
