@@ -218,7 +218,7 @@ def time_decode_prep(ut, fg_mask, grid: int, dev, stream, C: int = 64) -> dict:
 def main():
     args = parse()
     if args.gpus != 1:
-        print(f"bench.py runs on one GPU; --gpus {args.gpus} is not supported in this build "
+        print(f"bench.py runs on one GPU; --gpus {args.gpus} is not supported "
               f"(the path would shard by heads; see the design notes).", file=sys.stderr)
         sys.exit(2)
     import numpy as np
