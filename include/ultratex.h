@@ -22,6 +22,11 @@
  *    returns UT_ERR_HIP with the HIP error text. No C++ exception crosses the
  *    ABI.
  *  - Token and block indices are int32; byte offsets are computed in 64 bits.
+ *  - Block lists passed to the attention calls are trusted. With the
+ *    environment variable UT_VALIDATE set (to anything but "0") those calls
+ *    first copy the lists to the host, waiting for the stream, and return
+ *    UT_ERR_INVALID_ARG unless every row is strictly ascending within
+ *    [0, Nk) and the pointer array starts at 0 and never decreases.
  *  - bf16 is IEEE binary32 truncated to its upper 16 bits (stored as uint16),
  *    results rounded to nearest even.
  */

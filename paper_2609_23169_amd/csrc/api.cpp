@@ -4,7 +4,9 @@
 #include <cmath>
 #include <cstdarg>
 #include <cstdio>
+#include <cstdlib>
 #include <cstring>
+#include <vector>
 
 #include "common.h"
 
@@ -174,6 +176,48 @@ ut_status ut_build_block_index(const uint8_t* block_mask, int32_t B, int32_t H, 
   return UT_OK;
 }
 
+namespace {
+// Opt-in checking of the block lists' contents (environment UT_VALIDATE set to
+// anything but "0"): a debugging aid, since it waits for the stream.
+bool validate_mode() {
+  const char* e = std::getenv("UT_VALIDATE");
+  return e && e[0] && !(e[0] == '0' && e[1] == 0);
+}
+
+// Copies a compressed list pair to the host and checks it: ptr[0] = 0, ptr
+// non-decreasing, and each row's entries strictly ascending in [0, limit).
+ut_status validate_lists(const char* fn, const char* what, const int32_t* ptr, const int32_t* idx,
+                         int64_t rows, int32_t limit, hipStream_t stream) {
+  std::vector<int32_t> p((size_t)rows + 1);
+  UT_TRY(check_hip(hipMemcpyAsync(p.data(), ptr, p.size() * sizeof(int32_t), hipMemcpyDeviceToHost,
+                                  stream),
+                   "validate copy"));
+  UT_TRY(check_hip(hipStreamSynchronize(stream), "validate sync"));
+  if (p[0] != 0) return fail(UT_ERR_INVALID_ARG, "%s: %s: pointers start at %d, not 0", fn, what, p[0]);
+  for (int64_t r = 0; r < rows; ++r)
+    if (p[r + 1] < p[r])
+      return fail(UT_ERR_INVALID_ARG, "%s: %s: pointers decrease at row %lld", fn, what,
+                  (long long)r);
+  std::vector<int32_t> v((size_t)p[rows]);
+  if (!v.empty()) {
+    UT_TRY(check_hip(hipMemcpyAsync(v.data(), idx, v.size() * sizeof(int32_t),
+                                    hipMemcpyDeviceToHost, stream),
+                     "validate copy"));
+    UT_TRY(check_hip(hipStreamSynchronize(stream), "validate sync"));
+  }
+  for (int64_t r = 0; r < rows; ++r)
+    for (int64_t e = p[r]; e < p[r + 1]; ++e) {
+      if (v[e] < 0 || v[e] >= limit)
+        return fail(UT_ERR_INVALID_ARG, "%s: %s: row %lld holds %d, outside [0, %d)", fn, what,
+                    (long long)r, v[e], limit);
+      if (e > p[r] && v[e] <= v[e - 1])
+        return fail(UT_ERR_INVALID_ARG, "%s: %s: row %lld is not strictly ascending", fn, what,
+                    (long long)r);
+    }
+  return UT_OK;
+}
+}  // namespace
+
 ut_status ut_bsattn_fwd(const void* q, const void* k, const void* v, void* o, float* lse,
                         int32_t B, int32_t N, int32_t H, int32_t D, int32_t block,
                         const int32_t* q_rowptr, const int32_t* q_cols, float softmax_scale,
@@ -189,6 +233,9 @@ ut_status ut_bsattn_fwd(const void* q, const void* k, const void* v, void* o, fl
   UT_TRY(check_ptr(fn, "q_rowptr", q_rowptr, 4));
   UT_TRY(check_ptr(fn, "q_cols", q_cols, 4));
   const AttnShape sh{B, N, H, D, block, (N + block - 1) / block, softmax_scale};
+  if (validate_mode())
+    UT_TRY(validate_lists(fn, "row lists", q_rowptr, q_cols, (int64_t)B * H * sh.nblk, sh.nblk,
+                          stream));
   return check_hip(launch_bsattn_fwd(q, k, v, o, lse, sh, q_rowptr, q_cols, stream),
                    "forward launch");
 }
@@ -219,6 +266,12 @@ ut_status ut_bsattn_bwd(const void* q, const void* k, const void* v, const void*
                 workspace ? workspace_bytes : (size_t)0);
   UT_TRY(check_ptr(fn, "workspace", workspace, 16));
   const AttnShape sh{B, N, H, D, block, (N + block - 1) / block, softmax_scale};
+  if (validate_mode()) {
+    UT_TRY(validate_lists(fn, "row lists", q_rowptr, q_cols, (int64_t)B * H * sh.nblk, sh.nblk,
+                          stream));
+    UT_TRY(validate_lists(fn, "column lists", kv_colptr, kv_rows, (int64_t)B * H * sh.nblk,
+                          sh.nblk, stream));
+  }
   return check_hip(launch_bsattn_bwd(q, k, v, o, dout, lse, dq, dk, dv, sh, q_rowptr, q_cols,
                                      kv_colptr, kv_rows, static_cast<float*>(workspace), stream),
                    "backward launch");

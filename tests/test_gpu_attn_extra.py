@@ -1,0 +1,111 @@
+"""More attention checks through the C ABI: a diagonal-only mask, gradient
+invariants at a mid size and at the full 2K size, the opt-in block-list
+validation mode, and launches on a non-default stream."""
+import math
+
+import numpy as np
+import pytest
+import torch
+
+import oracle
+import paper_2609_23169_amd as ut
+import workloads as W
+from parity import check_grad, check_out
+
+pytestmark = pytest.mark.gpu
+DEV = "cuda"
+
+
+def _run(case):
+    q, k, v, do = (case[n].to(DEV) for n in ("q", "k", "v", "do"))
+    idx = ut.build_block_index(torch.from_numpy(case["block_mask"]).to(DEV))
+    o, lse = ut.bsattn_fwd(q, k, v, idx, case["block"], case["scale"])
+    dq, dk, dv = ut.bsattn_bwd(q, k, v, o, do, lse, idx, case["block"], case["scale"])
+    torch.cuda.synchronize()
+    return q, k, v, do, idx, o, lse, dq, dk, dv
+
+
+def test_diagonal_only_mask_is_blockwise_dense_attention():
+    case = W.random_case(31, 900, 2, 128, 128, 0.0, diag=True)
+    *_, o, lse, dq, dk, dv = _run(case)
+    O, L = oracle.bsattn_fwd(case["q"], case["k"], case["v"], case["block_mask"], 128, case["scale"])
+    check_out(o, lse, O, L, "diagonal")
+    dQ, dK, dV = oracle.bsattn_bwd(case["q"], case["k"], case["v"], case["do"], case["block_mask"], 128,
+                                   case["scale"])
+    for got, ref, nm in ((dq, dQ, "dq"), (dk, dK, "dk"), (dv, dV, "dv")):
+        check_grad(got, ref, f"diagonal {nm}")
+
+
+def _invariants(dk, dv, do, label):
+    """Per head: sum over tokens of dK is 0 (rows of dS sum to 0) and of dV is
+    that of dO (rows of P sum to 1). P and dS enter the second products as bf16
+    (relative 2^-9 each) and the outputs are bf16, hence the 1e-2 bound
+    relative to the summed magnitudes."""
+    dk, dv, do = (t.float() for t in (dk, dv, do))
+    sk = dk.sum(dim=1).abs().amax().item()
+    ak = dk.abs().sum(dim=1).amin().item()
+    assert sk <= 1e-2 * ak, f"{label}: |sum dK| {sk:.3e} vs sum |dK| {ak:.3e}"
+    dd = (dv.sum(dim=1) - do.sum(dim=1)).abs().amax().item()
+    ao = do.abs().sum(dim=1).amin().item()
+    assert dd <= 1e-2 * ao, f"{label}: |sum dV - sum dO| {dd:.3e} vs sum |dO| {ao:.3e}"
+
+
+def test_gradient_invariants_mid_size():
+    case = W.random_case(32, 5000, 3, 128, 128, 0.3)     # diagonal kept: no empty rows
+    q, k, v, do, idx, o, lse, dq, dk, dv = _run(case)
+    _invariants(dk, dv, do, "mid")
+
+
+def test_gradient_invariants_full_size():
+    inst = W.make(W.WORKLOADS["c2k_train"].with_rho("0.1"), with_qkv=True, with_do=True)
+    case = {"q": inst.q, "k": inst.k, "v": inst.v, "do": inst.do, "block_mask": inst.block_mask,
+            "block": 128, "scale": 1 / math.sqrt(128)}
+    q, k, v, do, idx, o, lse, dq, dk, dv = _run(case)
+    _invariants(dk, dv, do, "2K")
+
+
+def test_validate_mode(monkeypatch):
+    case = W.random_case(33, 700, 2, 64, 64, 0.4)
+    q, k, v, do, idx, o_ref, lse_ref, *_ = _run(case)
+    B, N, H, D = q.shape
+    nb = -(-N // 64)
+    o, lse = torch.empty_like(q), torch.empty((B, H, N), dtype=torch.float32, device=DEV)
+    monkeypatch.setenv("UT_VALIDATE", "1")
+    # valid lists pass and give the same result
+    assert ut.ut_bsattn_fwd(q, k, v, o, lse, 64, idx["q_rowptr"], idx["q_cols"], case["scale"]) == ut.UT_OK
+    torch.cuda.synchronize()
+    assert torch.equal(o, o_ref) and torch.equal(lse, lse_ref)
+    # corrupted lists are refused before any launch
+    cols = idx["q_cols"].clone()
+    cols[3] = nb                                        # out of range
+    assert ut.ut_bsattn_fwd(q, k, v, o, lse, 64, idx["q_rowptr"], cols, case["scale"]) == ut.UT_ERR_INVALID_ARG
+    assert "outside" in ut.last_error()
+    rp = idx["q_rowptr"]
+    row = int(np.argmax(np.diff(rp.cpu().numpy()) >= 2))   # a row with two entries or more
+    cols = idx["q_cols"].clone()
+    a = int(rp[row].item())
+    cols[a], cols[a + 1] = cols[a + 1].clone(), cols[a].clone()   # not ascending
+    assert ut.ut_bsattn_fwd(q, k, v, o, lse, 64, rp, cols, case["scale"]) == ut.UT_ERR_INVALID_ARG
+    assert "ascending" in ut.last_error()
+    bad_rp = rp.clone()
+    bad_rp[5] = bad_rp[4] - 1                           # decreasing pointers
+    assert ut.ut_bsattn_fwd(q, k, v, o, lse, 64, bad_rp, idx["q_cols"], case["scale"]) == ut.UT_ERR_INVALID_ARG
+    ws = torch.empty(ut.ut_bsattn_bwd_workspace_size(B, N, H), dtype=torch.uint8, device=DEV)
+    dq, dk, dv = (torch.empty_like(q) for _ in range(3))
+    kvc = idx["kv_rows"].clone()
+    kvc[0] = -1
+    st = ut.ut_bsattn_bwd(q, k, v, o_ref, do, lse_ref, dq, dk, dv, 64, idx["q_rowptr"], idx["q_cols"],
+                          idx["kv_colptr"], kvc, case["scale"], ws)
+    assert st == ut.UT_ERR_INVALID_ARG and "column lists" in ut.last_error()
+
+
+def test_non_default_stream_matches_default():
+    case = W.random_case(34, 1500, 2, 128, 128, 0.3)
+    q, k, v, do, idx, o_ref, lse_ref, dq_ref, dk_ref, dv_ref = _run(case)
+    s = torch.cuda.Stream()
+    with torch.cuda.stream(s):
+        o, lse = ut.bsattn_fwd(q, k, v, idx, 128, case["scale"], stream=s)
+        dq, dk, dv = ut.bsattn_bwd(q, k, v, o, do, lse, idx, 128, case["scale"], stream=s)
+    s.synchronize()
+    for a, b in ((o, o_ref), (lse, lse_ref), (dq, dq_ref), (dk, dk_ref), (dv, dv_ref)):
+        assert torch.equal(a, b)
