@@ -34,6 +34,10 @@ Paper sections (arXiv 2609.23169, "UltraTex"):
     attention but prints no gradient formula; the oracle differentiates Eq. 8
     with the mask held constant (the standard softmax-attention gradient
     restricted to the retained pairs).
+  * Batches of differing lengths: training buckets samples by their
+    foreground token count (Sec. 4.1, Implementation Details), so the kept
+    counts within a batch are close but not equal. The reading taken: the
+    samples are packed back to back and each is its own Eq. 8 problem.
 """
 from __future__ import annotations
 
@@ -41,7 +45,7 @@ import numpy as np
 
 __all__ = [
     "compact", "gather", "scatter", "block_index",
-    "bsattn_fwd", "bsattn_bwd",
+    "bsattn_fwd", "bsattn_bwd", "bsattn_fwd_varlen", "bsattn_bwd_varlen",
     "block_pool", "topk_block_mask",
     "euler_update_fg", "fg_flow_loss",
     "composite_latent", "token_mask_from_alpha",
@@ -229,6 +233,59 @@ def bsattn_bwd(q, k, v, dout, block_mask, block: int, scale: float,
                 dV[b, keys, h, :] += P.T @ dOi
     return dQ, dK, dV
 
+
+
+def _varlen_samples(cu_seqlens, block: int):
+    """(b, first token, length, blocks) of each packed sample."""
+    cu = np.asarray(cu_seqlens, dtype=np.int64)
+    for b in range(cu.size - 1):
+        n = int(cu[b + 1] - cu[b])
+        yield b, int(cu[b]), n, -(-n // block)
+
+
+def bsattn_fwd_varlen(q, k, v, cu_seqlens, block_mask, block: int, scale: float):
+    """Eq. 8 over packed samples of differing lengths.
+
+    q, k, v: [T, H, D], sample b being tokens cu_seqlens[b] .. cu_seqlens[b+1]
+    - 1; block_mask: [B, H, Nb, Nb] for the longest sample. Sample b is the
+    uniform problem of `bsattn_fwd` on its own tokens with the leading
+    ceil(n_b / block) rows and columns of block_mask[b]; entries past them do
+    not exist for it and are ignored (reading taken). Tokens attend only
+    within their own sample. Returns (O [T, H, D], LSE [H, T]) in float64;
+    tokens outside every sample stay NaN.
+    """
+    Q, K, V = _f64(q), _f64(k), _f64(v)
+    m = np.asarray(block_mask)
+    T, H, D = Q.shape
+    O = np.full((T, H, D), np.nan)
+    LSE = np.full((H, T), np.nan)
+    for b, t0, n, nb in _varlen_samples(cu_seqlens, block):
+        if n == 0:
+            continue
+        sl = slice(t0, t0 + n)
+        Ob, Lb = bsattn_fwd(Q[None, sl], K[None, sl], V[None, sl], m[b:b + 1, :, :nb, :nb],
+                            block, scale)
+        O[sl] = Ob[0]
+        LSE[:, sl] = Lb[0]
+    return O, LSE
+
+
+def bsattn_bwd_varlen(q, k, v, dout, cu_seqlens, block_mask, block: int, scale: float):
+    """Gradients of `bsattn_fwd_varlen`: each sample's gradients are those of
+    its own uniform problem (`bsattn_bwd`). Returns (dQ, dK, dV) [T, H, D]
+    float64; tokens outside every sample stay NaN."""
+    Q, K, V, dO = _f64(q), _f64(k), _f64(v), _f64(dout)
+    m = np.asarray(block_mask)
+    out = [np.full(Q.shape, np.nan) for _ in range(3)]
+    for b, t0, n, nb in _varlen_samples(cu_seqlens, block):
+        if n == 0:
+            continue
+        sl = slice(t0, t0 + n)
+        grads = bsattn_bwd(Q[None, sl], K[None, sl], V[None, sl], dO[None, sl],
+                           m[b:b + 1, :, :nb, :nb], block, scale)
+        for g, full in zip(grads, out):
+            full[sl] = g[0]
+    return tuple(out)
 
 
 # ---------------------------------------------------------------------------

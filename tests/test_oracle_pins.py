@@ -595,3 +595,81 @@ def test_topk_dense_prefix_blocks():
     # P = 0 is the plain selection; a prefix covering everything keeps all
     assert np.array_equal(oracle.topk_block_mask(q, k, block, kk, 0)[0], oracle.topk_block_mask(q, k, block, kk)[0])
     assert oracle.topk_block_mask(q, k, block, kk, nb)[0].all()
+
+
+# ---------------------------------------------------------------------------
+# Packed samples of differing lengths (Eq. 8 per sample)
+# ---------------------------------------------------------------------------
+
+def _packed_token_mask(cu, bm, block, H):
+    """Token-level mask [1, H, T, T] of the whole packed sequence: a pair is
+    allowed only inside one sample, and there only where that sample's block
+    mask holds (block coordinates measured from the sample's first token)."""
+    T = int(cu[-1])
+    allow = np.zeros((1, H, T, T), dtype=bool)
+    for b in range(len(cu) - 1):
+        t0, t1 = int(cu[b]), int(cu[b + 1])
+        blk = (np.arange(t0, t1) - t0) // block
+        for h in range(H):
+            allow[0, h, t0:t1, t0:t1] = bm[b, h][np.ix_(blk, blk)].astype(bool)
+    return allow
+
+
+def _varlen_case(seed, lens, block, H, D, density):
+    rng = np.random.default_rng(seed)
+    cu = np.concatenate([[0], np.cumsum(lens)]).astype(np.int64)
+    T, nb = int(cu[-1]), -(-max(lens) // block)
+    q, k, v, do = (rng.standard_normal((T, H, D)) for _ in range(4))
+    # random blocks everywhere (entries past a sample's own blocks included,
+    # which must be ignored) and the diagonal within each sample, so that no
+    # row of the dense reference is fully masked
+    bm = (rng.random((len(lens), H, nb, nb)) < density).astype(np.uint8)
+    for b, n in enumerate(lens):
+        d = np.arange(-(-n // block))
+        bm[b][:, d, d] = 1
+    return cu, q, k, v, do, bm
+
+
+@pytest.mark.parametrize("seed,lens,block,H,D", [(1, [37, 70, 16], 16, 2, 8),
+                                                 (2, [5, 0, 64, 33], 16, 1, 4),
+                                                 (3, [100, 99], 32, 2, 16)])
+def test_varlen_fwd_bwd_match_block_diagonal_dense_attention(seed, lens, block, H, D):
+    """The packed sequence as ONE dense attention problem whose token mask is
+    block-diagonal over the samples: torch's SDPA and autograd in float64
+    must reproduce the per-sample oracle (a wrong offset, a leak across
+    samples or a mask entry read in the wrong sample's frame fails this)."""
+    cu, q, k, v, do, bm = _varlen_case(seed, lens, block, H, D, 0.4)
+    scale = 1.0 / math.sqrt(D)
+    O, L = oracle.bsattn_fwd_varlen(q, k, v, cu, bm, block, scale)
+    allow = torch.as_tensor(_packed_token_mask(cu, bm, block, H))
+    tq, tk, tv = (torch.tensor(a[None], requires_grad=True) for a in (q, k, v))
+    t = lambda a: a.permute(0, 2, 1, 3)
+    o = torch.nn.functional.scaled_dot_product_attention(t(tq), t(tk), t(tv), attn_mask=allow)
+    o = o.permute(0, 2, 1, 3)
+    assert np.allclose(O, o[0].detach().numpy(), atol=1e-12)
+    s = torch.einsum("nhd,mhd->hnm", torch.tensor(q), torch.tensor(k)) * scale
+    lse = torch.logsumexp(s.masked_fill(~allow[0], -math.inf), dim=-1).numpy()
+    assert np.allclose(L, lse, atol=1e-12)
+    o.backward(torch.tensor(do[None]))
+    dQ, dK, dV = oracle.bsattn_bwd_varlen(q, k, v, do, cu, bm, block, scale)
+    assert np.allclose(dQ, tq.grad[0].numpy(), atol=1e-12)
+    assert np.allclose(dK, tk.grad[0].numpy(), atol=1e-12)
+    assert np.allclose(dV, tv.grad[0].numpy(), atol=1e-12)
+
+
+def test_varlen_samples_are_independent():
+    """Changing one sample's tokens leaves every other sample's outputs and
+    gradients exactly as they were."""
+    cu, q, k, v, do, bm = _varlen_case(7, [40, 23, 57], 16, 2, 8, 0.5)
+    base = oracle.bsattn_fwd_varlen(q, k, v, cu, bm, 16, 0.3)[0]
+    gbase = oracle.bsattn_bwd_varlen(q, k, v, do, cu, bm, 16, 0.3)
+    q2, k2, v2 = q.copy(), k.copy(), v.copy()
+    for a in (q2, k2, v2):
+        a[40:63] += 5.0
+    O2 = oracle.bsattn_fwd_varlen(q2, k2, v2, cu, bm, 16, 0.3)[0]
+    g2 = oracle.bsattn_bwd_varlen(q2, k2, v2, do, cu, bm, 16, 0.3)
+    others = np.r_[0:40, 63:120]
+    assert np.array_equal(O2[others], base[others])
+    assert not np.allclose(O2[40:63], base[40:63])
+    for a, b in zip(g2, gbase):
+        assert np.array_equal(a[others], b[others])
