@@ -197,6 +197,50 @@ ut_status ut_bsattn_bwd(const void* q, const void* k, const void* v,
                         size_t workspace_bytes, hipStream_t stream);
 
 /* ------------------------------------------------------------------------
+ * Variable-length batches of the two attention calls: B samples of differing
+ * kept-token counts packed back to back in one launch. The paper buckets
+ * training samples by their foreground token count (Sec. 4.1, Implementation
+ * Details) because the count differs from asset to asset; packing lets one
+ * launch serve a bucket whose counts still differ. Each sample attends only
+ * within itself, with the same math as ut_bsattn_fwd / ut_bsattn_bwd.
+ *
+ * q, k, v, o, dout, dq, dk, dv  bf16 [T, H, D]: sample b holds tokens
+ *           [cu_seqlens[b], cu_seqlens[b+1]).
+ * cu_seqlens  device int32 [B + 1], 0 = cu[0] <= cu[1] <= ... <= cu[B] = T.
+ * T         packed tokens (int64, below 2^31; T = 0 launches nothing).
+ * max_seqlen  >= every sample's length; sizes the block grid:
+ *           Nb = ceil(max_seqlen / block) blocks per sample.
+ * lse       fp32 [H, T] (head-major over the packed tokens).
+ * q_rowptr, q_cols (and kv_colptr, kv_rows)  lists of ut_build_block_index
+ *           over a [B, H, Nb, Nb] block mask. Sample b uses its leading
+ *           ceil(len_b / block) block rows and columns; list entries past
+ *           them are ignored, and its last block may be short.
+ * workspace (backward) ut_bsattn_bwd_varlen_workspace_size(T, H) bytes.
+ * Offsets are clamped to [0, T] and lengths to max_seqlen inside the
+ * kernels, so bad offsets cannot reach outside the tensors; tokens covered by
+ * no sample are left unwritten. With UT_VALIDATE set, cu_seqlens is checked
+ * as described above (UT_ERR_INVALID_ARG otherwise).
+ * Errors: as the uniform calls, with max_seqlen in the role of N.
+ * ---------------------------------------------------------------------- */
+ut_status ut_bsattn_fwd_varlen(const void* q, const void* k, const void* v,
+                               void* o, float* lse, const int32_t* cu_seqlens,
+                               int32_t B, int64_t T, int32_t max_seqlen,
+                               int32_t H, int32_t D, int32_t block,
+                               const int32_t* q_rowptr, const int32_t* q_cols,
+                               float softmax_scale, hipStream_t stream);
+size_t ut_bsattn_bwd_varlen_workspace_size(int64_t T, int32_t H);
+ut_status ut_bsattn_bwd_varlen(const void* q, const void* k, const void* v,
+                               const void* o, const void* dout,
+                               const float* lse, void* dq, void* dk, void* dv,
+                               const int32_t* cu_seqlens, int32_t B, int64_t T,
+                               int32_t max_seqlen, int32_t H, int32_t D,
+                               int32_t block, const int32_t* q_rowptr,
+                               const int32_t* q_cols, const int32_t* kv_colptr,
+                               const int32_t* kv_rows, float softmax_scale,
+                               void* workspace, size_t workspace_bytes,
+                               hipStream_t stream);
+
+/* ------------------------------------------------------------------------
  * Top-K block selection (Sec. 3.3, Eq. 6 and Eq. 7): the block mask M_c of
  * block-sparse attention from mean-pooled query and key blocks. Per (b, h),
  * pool(X)_i is the mean of block i's token rows (a short last block averages

@@ -32,6 +32,7 @@ EXPORTS = [
     "ut_drop_background_workspace_size", "ut_drop_background",
     "ut_scatter_foreground", "ut_build_block_index",
     "ut_bsattn_fwd", "ut_bsattn_bwd_workspace_size", "ut_bsattn_bwd",
+    "ut_bsattn_fwd_varlen", "ut_bsattn_bwd_varlen_workspace_size", "ut_bsattn_bwd_varlen",
     "ut_topk_block_mask_workspace_size", "ut_topk_block_mask",
     "ut_euler_update_foreground", "ut_fg_flow_loss_workspace_size", "ut_fg_flow_loss",
     "ut_composite_latent", "ut_token_mask_workspace_size", "ut_token_mask_from_alpha",
@@ -57,6 +58,11 @@ _SIGS = {
     "ut_bsattn_bwd_workspace_size": (_sz, [_i32, _i32, _i32]),
     "ut_bsattn_bwd": (_c.c_int, [_vp, _vp, _vp, _vp, _vp, _vp, _vp, _vp, _vp, _i32, _i32, _i32, _i32, _i32,
                                  _vp, _vp, _vp, _vp, _f32, _vp, _sz, _vp]),
+    "ut_bsattn_fwd_varlen": (_c.c_int, [_vp, _vp, _vp, _vp, _vp, _vp, _i32, _i64, _i32, _i32, _i32, _i32,
+                                        _vp, _vp, _f32, _vp]),
+    "ut_bsattn_bwd_varlen_workspace_size": (_sz, [_i64, _i32]),
+    "ut_bsattn_bwd_varlen": (_c.c_int, [_vp, _vp, _vp, _vp, _vp, _vp, _vp, _vp, _vp, _vp, _i32, _i64, _i32,
+                                        _i32, _i32, _i32, _vp, _vp, _vp, _vp, _f32, _vp, _sz, _vp]),
     "ut_topk_block_mask_workspace_size": (_sz, [_i32, _i32, _i32, _i32, _i32]),
     "ut_topk_block_mask": (_c.c_int, [_vp, _vp, _i32, _i32, _i32, _i32, _i32, _i32, _i32, _vp, _vp, _sz,
                                       _vp]),
@@ -221,6 +227,51 @@ def ut_bsattn_bwd(q, k, v, o, dout, lse, dq, dk, dv, block: int, q_rowptr, q_col
                                _p(kv_rows), softmax_scale, _p(workspace), ws_bytes, _stream(stream))
 
 
+def _check_varlen(q, k, v, cu_seqlens, max_seqlen, block, rowptr, cols):
+    _need(q.dim() == 3, "q: bf16 [T, H, D] (packed samples)")
+    T, H, D = q.shape
+    for t in (q, k, v):
+        _need(t.shape == q.shape and t.dtype == torch.bfloat16, "q, k, v: bf16 [T,H,D], same shape")
+    _need(cu_seqlens.dtype == torch.int32 and cu_seqlens.dim() == 1 and cu_seqlens.numel() >= 2,
+          "cu_seqlens: int32 [B+1]")
+    B = cu_seqlens.numel() - 1
+    _need(block > 0 and max_seqlen > 0, "block and max_seqlen must be positive")
+    nb = -(-max_seqlen // block)
+    _need(rowptr.dtype == torch.int32 and rowptr.numel() >= B * H * nb + 1, "rowptr int32 [B*H*Nb+1]")
+    _need(cols.dtype == torch.int32, "cols int32")
+    return B, T, H, D, nb
+
+
+def ut_bsattn_fwd_varlen(q, k, v, o, lse, cu_seqlens, max_seqlen: int, block: int, q_rowptr, q_cols,
+                         softmax_scale: float, stream=None) -> int:
+    B, T, H, D, nb = _check_varlen(q, k, v, cu_seqlens, max_seqlen, block, q_rowptr, q_cols)
+    _need(o.shape == q.shape and o.dtype == torch.bfloat16, "o: bf16 [T,H,D]")
+    _need(lse.dtype == torch.float32 and lse.numel() >= H * T, "lse: fp32 [H,T]")
+    return lib().ut_bsattn_fwd_varlen(_p(q), _p(k), _p(v), _p(o), _p(lse), _p(cu_seqlens), B, T,
+                                      max_seqlen, H, D, block, _p(q_rowptr), _p(q_cols), softmax_scale,
+                                      _stream(stream))
+
+
+def ut_bsattn_bwd_varlen_workspace_size(T: int, H: int) -> int:
+    return int(lib().ut_bsattn_bwd_varlen_workspace_size(T, H))
+
+
+def ut_bsattn_bwd_varlen(q, k, v, o, dout, lse, dq, dk, dv, cu_seqlens, max_seqlen: int, block: int,
+                         q_rowptr, q_cols, kv_colptr, kv_rows, softmax_scale: float, workspace,
+                         stream=None) -> int:
+    B, T, H, D, nb = _check_varlen(q, k, v, cu_seqlens, max_seqlen, block, q_rowptr, q_cols)
+    for t in (o, dout, dq, dk, dv):
+        _need(t.shape == q.shape and t.dtype == torch.bfloat16, "o, dout, dq, dk, dv: bf16 [T,H,D]")
+    _need(lse.dtype == torch.float32 and lse.numel() >= H * T, "lse: fp32 [H,T]")
+    _need(kv_colptr.dtype == torch.int32 and kv_colptr.numel() >= B * H * nb + 1, "kv_colptr int32")
+    _need(kv_rows.dtype == torch.int32, "kv_rows int32")
+    ws_bytes = _nbytes(workspace) if workspace is not None else 0
+    return lib().ut_bsattn_bwd_varlen(_p(q), _p(k), _p(v), _p(o), _p(dout), _p(lse), _p(dq), _p(dk),
+                                      _p(dv), _p(cu_seqlens), B, T, max_seqlen, H, D, block,
+                                      _p(q_rowptr), _p(q_cols), _p(kv_colptr), _p(kv_rows),
+                                      softmax_scale, _p(workspace), ws_bytes, _stream(stream))
+
+
 def ut_topk_block_mask_workspace_size(B: int, N: int, H: int, D: int, block: int) -> int:
     return int(lib().ut_topk_block_mask_workspace_size(B, N, H, D, block))
 
@@ -369,6 +420,33 @@ def bsattn_bwd(q, k, v, o, dout, lse, index, block: int, softmax_scale: float, w
     _raise("ut_bsattn_bwd", ut_bsattn_bwd(q, k, v, o, dout, lse, dq, dk, dv, block,
                                           index["q_rowptr"], index["q_cols"], index["kv_colptr"],
                                           index["kv_rows"], softmax_scale, workspace, stream))
+    return dq, dk, dv
+
+
+def bsattn_fwd_varlen(q, k, v, cu_seqlens, max_seqlen: int, index, block: int, softmax_scale: float,
+                      stream=None):
+    """Packed samples q, k, v [T, H, D]; index over a [B, H, Nb, Nb] block
+    mask, Nb = ceil(max_seqlen / block). Returns (o [T, H, D], lse [H, T])."""
+    T, H, D = q.shape
+    o = torch.zeros_like(q)
+    lse = torch.empty((H, T), dtype=torch.float32, device=q.device)
+    _raise("ut_bsattn_fwd_varlen",
+           ut_bsattn_fwd_varlen(q, k, v, o, lse, cu_seqlens, max_seqlen, block, index["q_rowptr"],
+                                index["q_cols"], softmax_scale, stream))
+    return o, lse
+
+
+def bsattn_bwd_varlen(q, k, v, o, dout, lse, cu_seqlens, max_seqlen: int, index, block: int,
+                      softmax_scale: float, workspace=None, stream=None):
+    T, H, D = q.shape
+    dq, dk, dv = torch.zeros_like(q), torch.zeros_like(q), torch.zeros_like(q)
+    if workspace is None:
+        workspace = torch.empty(max(ut_bsattn_bwd_varlen_workspace_size(T, H), 16), dtype=torch.uint8,
+                                device=q.device)
+    _raise("ut_bsattn_bwd_varlen",
+           ut_bsattn_bwd_varlen(q, k, v, o, dout, lse, dq, dk, dv, cu_seqlens, max_seqlen, block,
+                                index["q_rowptr"], index["q_cols"], index["kv_colptr"], index["kv_rows"],
+                                softmax_scale, workspace, stream))
     return dq, dk, dv
 
 

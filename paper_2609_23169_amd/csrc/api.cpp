@@ -232,7 +232,8 @@ ut_status ut_bsattn_fwd(const void* q, const void* k, const void* v, void* o, fl
   UT_TRY(check_ptr(fn, "lse", lse, 4));
   UT_TRY(check_ptr(fn, "q_rowptr", q_rowptr, 4));
   UT_TRY(check_ptr(fn, "q_cols", q_cols, 4));
-  const AttnShape sh{B, N, H, D, block, (N + block - 1) / block, softmax_scale};
+  const AttnShape sh{B, N, H, D, block, (N + block - 1) / block, softmax_scale, nullptr,
+                     (int64_t)B * N};
   if (validate_mode())
     UT_TRY(validate_lists(fn, "row lists", q_rowptr, q_cols, (int64_t)B * H * sh.nblk, sh.nblk,
                           stream));
@@ -265,7 +266,107 @@ ut_status ut_bsattn_bwd(const void* q, const void* k, const void* v, const void*
     return fail(UT_ERR_WORKSPACE, "%s: workspace of %zu bytes required (got %zu)", fn, need,
                 workspace ? workspace_bytes : (size_t)0);
   UT_TRY(check_ptr(fn, "workspace", workspace, 16));
-  const AttnShape sh{B, N, H, D, block, (N + block - 1) / block, softmax_scale};
+  const AttnShape sh{B, N, H, D, block, (N + block - 1) / block, softmax_scale, nullptr,
+                     (int64_t)B * N};
+  if (validate_mode()) {
+    UT_TRY(validate_lists(fn, "row lists", q_rowptr, q_cols, (int64_t)B * H * sh.nblk, sh.nblk,
+                          stream));
+    UT_TRY(validate_lists(fn, "column lists", kv_colptr, kv_rows, (int64_t)B * H * sh.nblk,
+                          sh.nblk, stream));
+  }
+  return check_hip(launch_bsattn_bwd(q, k, v, o, dout, lse, dq, dk, dv, sh, q_rowptr, q_cols,
+                                     kv_colptr, kv_rows, static_cast<float*>(workspace), stream),
+                   "backward launch");
+}
+
+namespace {
+// Sample offsets of the variable-length calls: B + 1 device int32 values.
+// Under UT_VALIDATE they are copied to the host and must start at 0, end at
+// T and never decrease, with no sample longer than max_seqlen.
+ut_status check_varlen(const char* fn, const int32_t* cu_seqlens, int32_t B, int64_t T,
+                       int32_t max_seqlen, hipStream_t stream) {
+  UT_TRY(check_ptr(fn, "cu_seqlens", cu_seqlens, 4));
+  if (T < 0 || T >= ((int64_t)1 << 31))
+    return fail(UT_ERR_INVALID_ARG, "%s: T = %lld outside [0, 2^31)", fn, (long long)T);
+  if (!validate_mode()) return UT_OK;
+  std::vector<int32_t> cu((size_t)B + 1);
+  UT_TRY(check_hip(hipMemcpyAsync(cu.data(), cu_seqlens, cu.size() * sizeof(int32_t),
+                                  hipMemcpyDeviceToHost, stream),
+                   "validate copy"));
+  UT_TRY(check_hip(hipStreamSynchronize(stream), "validate sync"));
+  if (cu[0] != 0 || cu[B] != T)
+    return fail(UT_ERR_INVALID_ARG, "%s: cu_seqlens must run from 0 to T = %lld (got %d .. %d)",
+                fn, (long long)T, cu[0], cu[B]);
+  for (int32_t b = 0; b < B; ++b) {
+    if (cu[b + 1] < cu[b])
+      return fail(UT_ERR_INVALID_ARG, "%s: cu_seqlens decreases at sample %d", fn, b);
+    if (cu[b + 1] - cu[b] > max_seqlen)
+      return fail(UT_ERR_INVALID_ARG, "%s: sample %d has %d tokens > max_seqlen %d", fn, b,
+                  cu[b + 1] - cu[b], max_seqlen);
+  }
+  return UT_OK;
+}
+}  // namespace
+
+ut_status ut_bsattn_fwd_varlen(const void* q, const void* k, const void* v, void* o, float* lse,
+                               const int32_t* cu_seqlens, int32_t B, int64_t T,
+                               int32_t max_seqlen, int32_t H, int32_t D, int32_t block,
+                               const int32_t* q_rowptr, const int32_t* q_cols,
+                               float softmax_scale, hipStream_t stream) {
+  static const char* fn = "ut_bsattn_fwd_varlen";
+  g_last_error[0] = 0;
+  UT_TRY(check_attn_common(fn, B, max_seqlen, H, D, block, softmax_scale));
+  UT_TRY(check_varlen(fn, cu_seqlens, B, T, max_seqlen, stream));
+  if (T * H * D >= (int64_t)1 << 40) return fail(UT_ERR_INVALID_ARG, "%s: problem too large", fn);
+  if (T == 0) return UT_OK;
+  UT_TRY(check_ptr(fn, "q", q, 16));
+  UT_TRY(check_ptr(fn, "k", k, 16));
+  UT_TRY(check_ptr(fn, "v", v, 16));
+  UT_TRY(check_ptr(fn, "o", o, 16));
+  UT_TRY(check_ptr(fn, "lse", lse, 4));
+  UT_TRY(check_ptr(fn, "q_rowptr", q_rowptr, 4));
+  UT_TRY(check_ptr(fn, "q_cols", q_cols, 4));
+  const AttnShape sh{B, max_seqlen, H, D, block, (max_seqlen + block - 1) / block,
+                     softmax_scale, cu_seqlens, T};
+  if (validate_mode())
+    UT_TRY(validate_lists(fn, "row lists", q_rowptr, q_cols, (int64_t)B * H * sh.nblk, sh.nblk,
+                          stream));
+  return check_hip(launch_bsattn_fwd(q, k, v, o, lse, sh, q_rowptr, q_cols, stream),
+                   "forward launch");
+}
+
+size_t ut_bsattn_bwd_varlen_workspace_size(int64_t T, int32_t H) {
+  if (T < 1 || H < 1) return 0;
+  return (size_t)T * H * 2 * sizeof(float);
+}
+
+ut_status ut_bsattn_bwd_varlen(const void* q, const void* k, const void* v, const void* o,
+                               const void* dout, const float* lse, void* dq, void* dk, void* dv,
+                               const int32_t* cu_seqlens, int32_t B, int64_t T,
+                               int32_t max_seqlen, int32_t H, int32_t D, int32_t block,
+                               const int32_t* q_rowptr, const int32_t* q_cols,
+                               const int32_t* kv_colptr, const int32_t* kv_rows,
+                               float softmax_scale, void* workspace, size_t workspace_bytes,
+                               hipStream_t stream) {
+  static const char* fn = "ut_bsattn_bwd_varlen";
+  g_last_error[0] = 0;
+  UT_TRY(check_attn_common(fn, B, max_seqlen, H, D, block, softmax_scale));
+  UT_TRY(check_varlen(fn, cu_seqlens, B, T, max_seqlen, stream));
+  if (T * H * D >= (int64_t)1 << 40) return fail(UT_ERR_INVALID_ARG, "%s: problem too large", fn);
+  if (T == 0) return UT_OK;
+  const struct { const char* n; const void* p; uintptr_t a; } ptrs[] = {
+      {"q", q, 16},   {"k", k, 16},   {"v", v, 16},         {"o", o, 16},
+      {"dout", dout, 16}, {"lse", lse, 4}, {"dq", dq, 16},   {"dk", dk, 16},
+      {"dv", dv, 16}, {"q_rowptr", q_rowptr, 4}, {"q_cols", q_cols, 4},
+      {"kv_colptr", kv_colptr, 4}, {"kv_rows", kv_rows, 4}};
+  for (const auto& p : ptrs) UT_TRY(check_ptr(fn, p.n, p.p, p.a));
+  const size_t need = ut_bsattn_bwd_varlen_workspace_size(T, H);
+  if (!workspace || workspace_bytes < need)
+    return fail(UT_ERR_WORKSPACE, "%s: workspace of %zu bytes required (got %zu)", fn, need,
+                workspace ? workspace_bytes : (size_t)0);
+  UT_TRY(check_ptr(fn, "workspace", workspace, 16));
+  const AttnShape sh{B, max_seqlen, H, D, block, (max_seqlen + block - 1) / block,
+                     softmax_scale, cu_seqlens, T};
   if (validate_mode()) {
     UT_TRY(validate_lists(fn, "row lists", q_rowptr, q_cols, (int64_t)B * H * sh.nblk, sh.nblk,
                           stream));

@@ -68,4 +68,25 @@ __device__ inline void buffer_load_lds16(__amdgpu_buffer_rsrc_t rs, char* lds, i
                                            voffset, 0, 0, 0);
 }
 
+// Where sample b's rows live. Uniform batch (cu == nullptr): tokens
+// [b N, b N + N) of the packed [B N, H, D] tensors, per-row statistics (LSE
+// and its relatives) laid out [B, H, N]. Variable lengths: tokens
+// [cu[b], cu[b + 1]) and statistics laid out [H, T] over all T tokens.
+struct SampleRows {
+  int64_t tok0;    // first token of the sample
+  int n;           // its length
+  int64_t stat0;   // index of (head h, the sample's first token) in the statistics
+};
+// Offsets are clamped to [0, T] and lengths to N_all (the block grid's
+// extent), so no offsets can send an access outside the tensors.
+__device__ inline SampleRows sample_rows(const int32_t* __restrict__ cu, int64_t T, int b, int h,
+                                         int H, int N_all) {
+  if (cu) {
+    const int64_t t0 = min(max((int64_t)cu[b], (int64_t)0), T);
+    const int64_t t1 = min(max((int64_t)cu[b + 1], t0), T);
+    return SampleRows{t0, (int)min(t1 - t0, (int64_t)N_all), (int64_t)h * T + t0};
+  }
+  return SampleRows{(int64_t)b * N_all, N_all, ((int64_t)b * H + h) * N_all};
+}
+
 }  // namespace ut

@@ -32,16 +32,17 @@ namespace {
 constexpr float kLog2e = 1.4426950408889634f;
 
 // ---------------------------------------------------------------------------
-// prep: aux[(b H + h) N + n] = {LSE log2 e, rowsum(dO o O)}
+// prep: aux = {LSE log2 e, rowsum(dO o O)} per (head, token), in the layout of
+// LSE: [B, H, N] for a uniform batch, [H, T] over packed tokens otherwise
 // ---------------------------------------------------------------------------
 template <int D>
 __global__ __launch_bounds__(256) void bwd_prep_kernel(const __bf16* __restrict__ O,
                                                        const __bf16* __restrict__ dO,
                                                        const float* __restrict__ LSE,
-                                                       float2* __restrict__ aux, int B, int N,
-                                                       int H) {
+                                                       float2* __restrict__ aux, int64_t T_tok,
+                                                       int N, int H, bool packed) {
   constexpr int CPR = D / 8;  // lanes per (token, head) row
-  const int64_t rows = (int64_t)B * N * H;
+  const int64_t rows = T_tok * H;
   const int64_t gid = (int64_t)blockIdx.x * 256 + threadIdx.x;
   const int64_t row = gid / CPR;  // (b, n, h) in memory order
   const int c = (int)(gid % CPR);
@@ -56,9 +57,9 @@ __global__ __launch_bounds__(256) void bwd_prep_kernel(const __bf16* __restrict_
   for (int m = CPR / 2; m >= 1; m >>= 1) acc += __shfl_xor(acc, m, 64);
   if (row < rows && c == 0) {
     const int h = (int)(row % H);
-    const int64_t bn = row / H;
-    const int n = (int)(bn % N), b = (int)(bn / N);
-    const int64_t r = ((int64_t)b * H + h) * N + n;
+    const int64_t tok = row / H;
+    const int64_t r = packed ? (int64_t)h * T_tok + tok
+                             : ((tok / N) * H + h) * N + tok % N;
     aux[r] = make_float2(LSE[r] * kLog2e, acc);
   }
 }
@@ -112,8 +113,8 @@ template <int D, int BLOCK>
 __global__ __launch_bounds__(64 * (BLOCK / 32), (BLOCK == 128 || D == 64) ? 2 : 1) void bwd_dq_kernel(
     const __bf16* __restrict__ Q, const __bf16* __restrict__ K, const __bf16* __restrict__ V,
     const __bf16* __restrict__ dO, const float2* __restrict__ aux, __bf16* __restrict__ dQ, int B,
-    int N, int H, int nblk, float scale, const int32_t* __restrict__ rowptr,
-    const int32_t* __restrict__ cols) {
+    int N_all, int H, int nblk, float scale, const int32_t* __restrict__ rowptr,
+    const int32_t* __restrict__ cols, const int32_t* __restrict__ cu_seqlens, int64_t T_tok) {
   using C = BwdCfg<D, BLOCK, BLOCK / 32>;
   __shared__ __attribute__((aligned(1024))) char k_lds0[C::TILEB];
   __shared__ __attribute__((aligned(1024))) char k_lds1[C::TILEB];
@@ -128,9 +129,14 @@ __global__ __launch_bounds__(64 * (BLOCK / 32), (BLOCK == 128 || D == 64) ? 2 : 
   const int64_t bh = lt / nblk;
   const int h = (int)(bh % H), b = (int)(bh / H);
   const int64_t tok_stride = (int64_t)H * D;
-  const int64_t base_bh = (int64_t)b * N * tok_stride + (int64_t)h * D;
+  const SampleRows sr = sample_rows(cu_seqlens, T_tok, b, h, H, N_all);
+  const int N = sr.n;
+  if (N <= 0 || i * BLOCK >= N) return;
+  const int64_t base_bh = sr.tok0 * tok_stride + (int64_t)h * D;
   const int q = i * BLOCK + 32 * w + l32;
-  const int p0 = rowptr[lt], p1 = rowptr[lt + 1];
+  const int p0 = rowptr[lt];
+  int p1 = rowptr[lt + 1];
+  while (p1 > p0 && cols[p1 - 1] >= (N + BLOCK - 1) / BLOCK) --p1;   // past the sample
   const int T = (p1 - p0) * C::SUBS;
 
   f32x16 dqt[C::DT];
@@ -147,7 +153,7 @@ __global__ __launch_bounds__(64 * (BLOCK / 32), (BLOCK == 128 || D == 64) ? 2 : 
         doop[ks] = *reinterpret_cast<const bf16x8*>(dO + off + 16 * ks);
       }
     }
-    const float2 a2 = aux[bh * N + min(q, N - 1)];
+    const float2 a2 = aux[sr.stat0 + min(q, N - 1)];
     const float lse2 = a2.x, dl = a2.y;
     const LaneOffsets<C> lo(w, lane, tok_stride);
 
@@ -218,7 +224,7 @@ __global__ __launch_bounds__(64 * (BLOCK / 32), (BLOCK == 128 || D == 64) ? 2 : 
     load_tile(V, 0, v_lds0);
     __builtin_amdgcn_s_waitcnt(0);
     __syncthreads();
-    const bool tail = (N % BLOCK != 0) && cols[p1 - 1] == nblk - 1;
+    const bool tail = (N % BLOCK != 0) && cols[p1 - 1] == (N + BLOCK - 1) / BLOCK - 1;
     const int Tm = tail ? T - C::SUBS : T;
     using I0 = std::integral_constant<int, 0>;
     using I1 = std::integral_constant<int, 1>;
@@ -264,8 +270,9 @@ template <int D, int BLOCK>
 __global__ __launch_bounds__(128 * (BLOCK / 32), 1) void bwd_dkdv_kernel(
     const __bf16* __restrict__ Q, const __bf16* __restrict__ K, const __bf16* __restrict__ V,
     const __bf16* __restrict__ dO, const float2* __restrict__ aux, __bf16* __restrict__ dK,
-    __bf16* __restrict__ dV, int B, int N, int H, int nblk, float scale,
-    const int32_t* __restrict__ colptr, const int32_t* __restrict__ rows_list) {
+    __bf16* __restrict__ dV, int B, int N_all, int H, int nblk, float scale,
+    const int32_t* __restrict__ colptr, const int32_t* __restrict__ rows_list,
+    const int32_t* __restrict__ cu_seqlens, int64_t T_tok) {
   constexpr int NK = BLOCK / 32;        // key groups (waves per query half)
   using C = BwdCfg<D, BLOCK, 2 * NK>;
   constexpr int AUXB = 1024;            // 64 rows x 8 bytes, padded to one load
@@ -287,9 +294,14 @@ __global__ __launch_bounds__(128 * (BLOCK / 32), 1) void bwd_dkdv_kernel(
   const int64_t bh = lt / nblk;
   const int h = (int)(bh % H), b = (int)(bh / H);
   const int64_t tok_stride = (int64_t)H * D;
-  const int64_t base_bh = (int64_t)b * N * tok_stride + (int64_t)h * D;
+  const SampleRows sr = sample_rows(cu_seqlens, T_tok, b, h, H, N_all);
+  const int N = sr.n;
+  if (N <= 0 || j * BLOCK >= N) return;   // uniform over the workgroup
+  const int64_t base_bh = sr.tok0 * tok_stride + (int64_t)h * D;
   const int key = j * BLOCK + 32 * kw + l32;
-  const int p0 = colptr[lt], p1 = colptr[lt + 1];
+  const int p0 = colptr[lt];
+  int p1 = colptr[lt + 1];
+  while (p1 > p0 && rows_list[p1 - 1] >= (N + BLOCK - 1) / BLOCK) --p1;   // past the sample
   const int T = (p1 - p0) * C::SUBS;
 
   f32x16 dkt[C::DT], dvt[C::DT];
@@ -331,7 +343,7 @@ __global__ __launch_bounds__(128 * (BLOCK / 32), 1) void bwd_dkdv_kernel(
       }
       if (w == 0) {   // rows past N (and lanes past the 64 rows) read zeros
         const __amdgpu_buffer_rsrc_t ra =
-            buffer_rsrc(aux + bh * N + r0, r0 < N ? min(N - r0, C::ST) * 8 : 0);
+            buffer_rsrc(aux + sr.stat0 + r0, r0 < N ? min(N - r0, C::ST) * 8 : 0);
         buffer_load_lds16(ra, ad, 16 * lane);
       }
     };
@@ -455,9 +467,9 @@ hipError_t launch_bwd_t(const void* q, const void* k, const void* v, const void*
                         const int32_t* colptr, const int32_t* rows, float* ws, hipStream_t s) {
   auto bf = [](const void* p) { return static_cast<const __bf16*>(p); };
   float2* aux = reinterpret_cast<float2*>(ws);
-  const int64_t rows_total = (int64_t)sh.B * sh.N * sh.H * (D / 8);
+  const int64_t rows_total = sh.T * sh.H * (D / 8);
   hipLaunchKernelGGL((bwd_prep_kernel<D>), dim3((unsigned)((rows_total + 255) / 256)), dim3(256), 0,
-                     s, bf(o), bf(dout), lse, aux, sh.B, sh.N, sh.H);
+                     s, bf(o), bf(dout), lse, aux, sh.T, sh.N, sh.H, sh.cu != nullptr);
   // One workgroup per (b, h, block) in plain order. Workgroups go round-robin
   // to the 8 XCDs, so all XCDs work on the same few heads at once (their K and
   // V stay in the shared last-level cache) and a run of heavy blocks is spread
@@ -465,10 +477,11 @@ hipError_t launch_bwd_t(const void* q, const void* k, const void* v, const void*
   const dim3 grid((unsigned)((int64_t)sh.B * sh.H * sh.nblk));
   hipLaunchKernelGGL((bwd_dkdv_kernel<D, BLOCK>), grid, dim3(128 * (BLOCK / 32)), 0, s,
                      bf(q), bf(k), bf(v), bf(dout), aux, static_cast<__bf16*>(dk),
-                     static_cast<__bf16*>(dv), sh.B, sh.N, sh.H, sh.nblk, sh.scale, colptr, rows);
+                     static_cast<__bf16*>(dv), sh.B, sh.N, sh.H, sh.nblk, sh.scale, colptr, rows,
+                     sh.cu, sh.T);
   hipLaunchKernelGGL((bwd_dq_kernel<D, BLOCK>), grid, dim3(64 * (BLOCK / 32)), 0, s,
                      bf(q), bf(k), bf(v), bf(dout), aux, static_cast<__bf16*>(dq), sh.B, sh.N, sh.H,
-                     sh.nblk, sh.scale, rowptr, cols);
+                     sh.nblk, sh.scale, rowptr, cols, sh.cu, sh.T);
   return hipGetLastError();
 }
 

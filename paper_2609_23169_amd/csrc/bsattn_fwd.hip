@@ -56,8 +56,9 @@ struct FwdCfg {
 template <int D, int BLOCK>
 __global__ __launch_bounds__(64 * (BLOCK / 32), (BLOCK == 128 || D == 64) ? 2 : 1) void bsattn_fwd_kernel(
     const __bf16* __restrict__ Q, const __bf16* __restrict__ K, const __bf16* __restrict__ V,
-    __bf16* __restrict__ O, float* __restrict__ LSE, int B, int N, int H, int nblk, float scale,
-    const int32_t* __restrict__ rowptr, const int32_t* __restrict__ cols) {
+    __bf16* __restrict__ O, float* __restrict__ LSE, int B, int N_all, int H, int nblk, float scale,
+    const int32_t* __restrict__ rowptr, const int32_t* __restrict__ cols,
+    const int32_t* __restrict__ cu_seqlens, int64_t T_tok) {
   using C = FwdCfg<D, BLOCK>;
   // Four LDS objects (K and V, two stages each): distinct objects let the
   // compiler see that a load into one never aliases reads of another.
@@ -74,10 +75,17 @@ __global__ __launch_bounds__(64 * (BLOCK / 32), (BLOCK == 128 || D == 64) ? 2 : 
   const int64_t bh = lt / nblk;
   const int h = (int)(bh % H), b = (int)(bh / H);
   const int64_t tok_stride = (int64_t)H * D;     // elements between tokens
-  const int64_t base_bh = (int64_t)b * N * tok_stride + (int64_t)h * D;
+  const SampleRows sr = sample_rows(cu_seqlens, T_tok, b, h, H, N_all);
+  const int N = sr.n;                            // this sample's tokens
+  if (N <= 0 || i * BLOCK >= N) return;         // no query rows of this sample here
+  const int64_t base_bh = sr.tok0 * tok_stride + (int64_t)h * D;
 
   const int q = i * BLOCK + 32 * w + l32;       // this lane's query row
-  const int p0 = rowptr[lt], p1 = rowptr[lt + 1];
+  const int p0 = rowptr[lt];
+  int p1 = rowptr[lt + 1];
+  // entries past the sample's last key block (possible only with variable
+  // lengths, where the block grid is sized for the longest) are ignored
+  while (p1 > p0 && cols[p1 - 1] >= (N + BLOCK - 1) / BLOCK) --p1;
   const int T = (p1 - p0) * C::SUBS;            // sub-tiles to visit (uniform)
 
   if (T == 0) {  // empty S_i: O = 0, LSE = -inf
@@ -88,7 +96,7 @@ __global__ __launch_bounds__(64 * (BLOCK / 32), (BLOCK == 128 || D == 64) ? 2 : 
 #pragma unroll
         for (int a = 0; a < 4; ++a)
           *reinterpret_cast<bf16x4*>(O + base_bh + q * tok_stride + 32 * dt + 8 * a + 4 * g) = z;
-      if (g == 0) LSE[bh * N + q] = -INFINITY;
+      if (g == 0) LSE[sr.stat0 + q] = -INFINITY;
     }
     return;
   }
@@ -237,7 +245,7 @@ __global__ __launch_bounds__(64 * (BLOCK / 32), (BLOCK == 128 || D == 64) ? 2 : 
 
   // The sub-tiles of a short last key block (always the end of the ascending
   // list) take the masked path.
-  const bool tail = (N % BLOCK != 0) && cols[p1 - 1] == nblk - 1;
+  const bool tail = (N % BLOCK != 0) && cols[p1 - 1] == (N + BLOCK - 1) / BLOCK - 1;
   const int Tm = tail ? T - C::SUBS : T;
   using I0 = std::integral_constant<int, 0>;
   using I1 = std::integral_constant<int, 1>;
@@ -274,7 +282,7 @@ __global__ __launch_bounds__(64 * (BLOCK / 32), (BLOCK == 128 || D == 64) ? 2 : 
         for (int e = 0; e < 4; ++e) v4[e] = (__bf16)(oacc[dt][4 * a + e] * inv);
         *reinterpret_cast<bf16x4*>(O + base_bh + q * tok_stride + 32 * dt + 8 * a + 4 * g) = v4;
       }
-    if (g == 0) LSE[bh * N + q] = l_tot > 0.f ? (m_run + __log2f(l_tot)) * kLn2 : -INFINITY;
+    if (g == 0) LSE[sr.stat0 + q] = l_tot > 0.f ? (m_run + __log2f(l_tot)) * kLn2 : -INFINITY;
   }
 }
 
@@ -290,7 +298,7 @@ hipError_t launch_fwd_t(const void* q, const void* k, const void* v, void* o, fl
   hipLaunchKernelGGL((bsattn_fwd_kernel<D, BLOCK>), grid, dim3(FwdCfg<D, BLOCK>::NT), 0,
                      s, static_cast<const __bf16*>(q), static_cast<const __bf16*>(k),
                      static_cast<const __bf16*>(v), static_cast<__bf16*>(o), lse, sh.B, sh.N, sh.H,
-                     sh.nblk, sh.scale, rowptr, cols);
+                     sh.nblk, sh.scale, rowptr, cols, sh.cu, sh.T);
   return hipGetLastError();
 }
 

@@ -31,8 +31,10 @@ hipError_t launch_block_index(const uint8_t* mask, int B, int H, int Nq, int Nk,
 
 // ---- Attention (bsattn_fwd.hip, bsattn_bwd.hip) ----
 struct AttnShape {
-  int B, N, H, D, block, nblk;
+  int B, N, H, D, block, nblk;   // N: tokens per sample (the longest, with cu)
   float scale;
+  const int32_t* cu = nullptr;   // [B + 1] sample offsets, or null for a uniform batch
+  int64_t T = 0;                 // packed tokens (B N when uniform)
 };
 hipError_t launch_bsattn_fwd(const void* q, const void* k, const void* v, void* o, float* lse,
                              const AttnShape& sh, const int32_t* rowptr, const int32_t* cols,

@@ -36,6 +36,8 @@ def test_workspace_sizes():
     assert ut.ut_drop_background_workspace_size(1) == 4
     assert ut.ut_drop_background_workspace_size(0) == 0
     assert ut.ut_bsattn_bwd_workspace_size(1, 77586, 24) == 77586 * 24 * 8
+    assert ut.ut_bsattn_bwd_varlen_workspace_size(77586, 24) == 77586 * 24 * 8
+    assert ut.ut_bsattn_bwd_varlen_workspace_size(0, 24) == 0
 
 
 def _fwd(**kw):
@@ -70,6 +72,48 @@ def test_bwd_rejects_missing_workspace():
     assert st == ut.UT_ERR_WORKSPACE
     args[2] = None
     assert lib.ut_bsattn_bwd(*args, FAKE, 1600, None) == ut.UT_ERR_INVALID_ARG
+
+
+def _fwd_varlen(**kw):
+    a = dict(q=FAKE, k=FAKE, v=FAKE, o=FAKE, lse=FAKE, cu=FAKE, B=3, T=300, maxlen=128, H=2, D=128,
+             block=128, rowptr=FAKE, cols=FAKE, scale=0.1)
+    a.update(kw)
+    return ut.lib().ut_bsattn_fwd_varlen(a["q"], a["k"], a["v"], a["o"], a["lse"], a["cu"], a["B"],
+                                         a["T"], a["maxlen"], a["H"], a["D"], a["block"], a["rowptr"],
+                                         a["cols"], a["scale"], None)
+
+
+@pytest.mark.parametrize("kw,status,msg", [
+    (dict(cu=None), ut.UT_ERR_INVALID_ARG, "cu_seqlens is NULL"),
+    (dict(T=-1), ut.UT_ERR_INVALID_ARG, "outside [0, 2^31)"),
+    (dict(T=1 << 31), ut.UT_ERR_INVALID_ARG, "outside [0, 2^31)"),
+    (dict(maxlen=0), ut.UT_ERR_INVALID_ARG, "must be >= 1"),
+    (dict(B=0), ut.UT_ERR_INVALID_ARG, "must be >= 1"),
+    (dict(D=96), ut.UT_ERR_UNSUPPORTED, "head_dim"),
+    (dict(q=None), ut.UT_ERR_INVALID_ARG, "q is NULL"),
+    (dict(lse=MISALIGNED), ut.UT_ERR_INVALID_ARG, "aligned"),
+])
+def test_fwd_varlen_rejects_bad_arguments(kw, status, msg):
+    assert _fwd_varlen(**kw) == status
+    assert msg in ut.last_error()
+
+
+def test_varlen_with_no_tokens_launches_nothing():
+    # T = 0: checked, then nothing to do (the fake pointers are never touched)
+    assert _fwd_varlen(T=0, q=None) == ut.UT_OK
+    lib = ut.lib()
+    args = [FAKE] * 10 + [3, 0, 128, 2, 128, 128] + [FAKE] * 4 + [0.1]
+    assert lib.ut_bsattn_bwd_varlen(*args, None, 0, None) == ut.UT_OK
+
+
+def test_bwd_varlen_rejects_missing_workspace():
+    lib = ut.lib()
+    args = [FAKE] * 10 + [3, 300, 128, 2, 128, 128] + [FAKE] * 4 + [0.1]
+    assert lib.ut_bsattn_bwd_varlen(*args, None, 0, None) == ut.UT_ERR_WORKSPACE
+    assert lib.ut_bsattn_bwd_varlen(*args, FAKE, 300 * 2 * 8 - 1, None) == ut.UT_ERR_WORKSPACE
+    args[9] = None
+    assert lib.ut_bsattn_bwd_varlen(*args, FAKE, 4800, None) == ut.UT_ERR_INVALID_ARG
+    assert "cu_seqlens" in ut.last_error()
 
 
 def test_drop_background_rejects_bad_arguments():

@@ -226,6 +226,41 @@ def random_case(seed: int, n: int, heads: int, head_dim: int, block: int,
             "block": block, "scale": 1.0 / math.sqrt(head_dim)}
 
 
+def varlen_case(seed: int, lens, heads: int, head_dim: int, block: int, density: float,
+                garbage_past_end: bool = True) -> dict:
+    """Seeded packed batch of samples with the given token counts: bf16
+    Q/K/V/dO [T, H, D] back to back, int32 offsets cu_seqlens [B + 1], and a
+    block mask [B, H, Nb, Nb] (Nb from the longest sample) with per-entry
+    density and the diagonal set within each sample. With garbage_past_end the
+    entries past a sample's own blocks are random too (they must be ignored);
+    otherwise they are 0."""
+    rng = np.random.default_rng(seed)
+    lens = [int(x) for x in lens]
+    cu = np.concatenate([[0], np.cumsum(lens)]).astype(np.int32)
+    T, nb = int(cu[-1]), max(1, -(-max(lens) // block))
+    q, k, v, do = (_bf16_normal(rng, (T, heads, head_dim)) for _ in range(4))
+    bm = (rng.random((len(lens), heads, nb, nb)) < density).astype(np.uint8)
+    for b, n in enumerate(lens):
+        own = -(-n // block)
+        if not garbage_past_end:
+            bm[b, :, own:, :] = 0
+            bm[b, :, :, own:] = 0
+        d = np.arange(own)
+        bm[b][:, d, d] = 1
+    return {"q": q, "k": k, "v": v, "do": do, "cu_seqlens": cu, "block_mask": bm,
+            "lens": lens, "max_seqlen": max(max(lens), 1), "block": block,
+            "scale": 1.0 / math.sqrt(head_dim)}
+
+
+def bucket_lengths(seed: int, wl: Workload, count: int) -> list:
+    """Kept-token counts of `count` samples of one foreground-count bucket of a
+    workload: each sample's count is its own draw of the workload's foreground
+    masks (Sec. 4.1 buckets training samples by this count). The counts are
+    sorted, as bucketing by count would order them."""
+    rng = np.random.default_rng(seed)
+    return sorted(int(fg_masks(wl, rng).sum()) for _ in range(count))
+
+
 def block_sizes(n: int, block: int) -> np.ndarray:
     """Real token count of each block of an N-token sequence (last may be short)."""
     nb = -(-n // block)
