@@ -183,7 +183,8 @@ ut_status ut_bsattn_fwd(const void* q, const void* k, const void* v, void* o,
  * q_rowptr, q_cols, kv_colptr, kv_rows  both lists of ut_build_block_index.
  * workspace         device scratch of ut_bsattn_bwd_workspace_size(B, N, H)
  *                   bytes (8 per query row), 16-byte aligned; holds the row
- *                   log-sum-exp in log2 units and delta = rowsum(dO o O).
+ *                   log-sum-exp in log2 units and -delta = -rowsum(dO o O)
+ *                   as two planes of 4 bytes per row.
  * Errors: as ut_bsattn_fwd, plus UT_ERR_WORKSPACE.
  * ---------------------------------------------------------------------- */
 size_t ut_bsattn_bwd_workspace_size(int32_t B, int32_t N, int32_t H);

@@ -2,7 +2,8 @@
 // Sec. 3.3) with the block mask held constant. Three launches, no atomics,
 // deterministic:
 //
-//   prep  : per query row, {LSE log2(e), delta = sum_d dO[r,d] O[r,d]} (fp32);
+//   prep  : per query row, LSE log2(e) and -delta = -sum_d dO[r,d] O[r,d]
+//           (fp32, two planes of the workspace);
 //   dQ    : one workgroup per (b, h, query block i), walking S_i (row lists).
 //           Each wave owns 32 queries, with its Q and dO rows as MFMA operands
 //           in registers. Per 64-key tile streamed through LDS:
@@ -12,8 +13,9 @@
 //           that select j (column lists). Waves w and w + BLOCK/32 own the
 //           same 32 keys (K rows in registers, V rows in LDS) and split each 64-row
 //           query tile between them: S = Q K^T and dP = dO V^T (lane = key
-//           column), dV^T += dO^T P and dK^T += Q^T dS with transposing LDS
-//           reads. The two partial sums meet once in LDS at the end.
+//           column; the dP accumulator starts at -delta, so it ends as
+//           dP - delta), dV^T += dO^T P and dK^T += Q^T dS with transposing
+//           LDS reads. The two partial sums meet once in LDS at the end.
 //
 // The dQ pass recomputes S and dP instead of accumulating dQ with atomics
 // from the dK/dV pass. Tiles go from global memory straight into LDS with
@@ -32,14 +34,15 @@ namespace {
 constexpr float kLog2e = 1.4426950408889634f;
 
 // ---------------------------------------------------------------------------
-// prep: aux = {LSE log2 e, rowsum(dO o O)} per (head, token), in the layout of
-// LSE: [B, H, N] for a uniform batch, [H, T] over packed tokens otherwise
+// prep: two planes over the statistics rows, in the layout of LSE ([B, H, N]
+// for a uniform batch, [H, T] over packed tokens otherwise):
+//   A[r] = LSE log2 e,   Dn[r] = -delta = -rowsum(dO o O)
 // ---------------------------------------------------------------------------
 template <int D>
 __global__ __launch_bounds__(256) void bwd_prep_kernel(const __bf16* __restrict__ O,
                                                        const __bf16* __restrict__ dO,
                                                        const float* __restrict__ LSE,
-                                                       float2* __restrict__ aux, int64_t T_tok,
+                                                       float* __restrict__ aux, int64_t T_tok,
                                                        int N, int H, bool packed) {
   constexpr int CPR = D / 8;  // lanes per (token, head) row
   const int64_t rows = T_tok * H;
@@ -60,7 +63,8 @@ __global__ __launch_bounds__(256) void bwd_prep_kernel(const __bf16* __restrict_
     const int64_t tok = row / H;
     const int64_t r = packed ? (int64_t)h * T_tok + tok
                              : ((tok / N) * H + h) * N + tok % N;
-    aux[r] = make_float2(LSE[r] * kLog2e, acc);
+    aux[r] = LSE[r] * kLog2e;
+    aux[rows + r] = -acc;
   }
 }
 
@@ -112,7 +116,7 @@ struct LaneOffsets {
 template <int D, int BLOCK>
 __global__ __launch_bounds__(64 * (BLOCK / 32), (BLOCK == 128 || D == 64) ? 2 : 1) void bwd_dq_kernel(
     const __bf16* __restrict__ Q, const __bf16* __restrict__ K, const __bf16* __restrict__ V,
-    const __bf16* __restrict__ dO, const float2* __restrict__ aux, __bf16* __restrict__ dQ, int B,
+    const __bf16* __restrict__ dO, const float* __restrict__ aux, __bf16* __restrict__ dQ, int B,
     int N_all, int H, int nblk, float scale, const int32_t* __restrict__ rowptr,
     const int32_t* __restrict__ cols, const int32_t* __restrict__ cu_seqlens, int64_t T_tok) {
   using C = BwdCfg<D, BLOCK, BLOCK / 32>;
@@ -153,8 +157,8 @@ __global__ __launch_bounds__(64 * (BLOCK / 32), (BLOCK == 128 || D == 64) ? 2 : 
         doop[ks] = *reinterpret_cast<const bf16x8*>(dO + off + 16 * ks);
       }
     }
-    const float2 a2 = aux[sr.stat0 + min(q, N - 1)];
-    const float lse2 = a2.x, dl = a2.y;
+    const int64_t ar = sr.stat0 + min(q, N - 1);
+    const float lse2 = aux[ar], ndl = aux[(int64_t)H * T_tok + ar];   // LSE log2 e, -delta
     const LaneOffsets<C> lo(w, lane, tok_stride);
 
     auto load_tile = [&](const __bf16* X, int t, char* dst) __attribute__((always_inline)) {
@@ -192,7 +196,7 @@ __global__ __launch_bounds__(64 * (BLOCK / 32), (BLOCK == 128 || D == 64) ? 2 : 
           float p = fast_exp2(__builtin_fmaf(s[kt][e], c2, -lse2));
           if constexpr (decltype(masked)::value)
             p = 32 * kt + 8 * (e >> 2) + 4 * g + (e & 3) >= lim ? 0.f : p;
-          dsb[kt][e >> 3][e & 7] = (__bf16)(p * (dp[kt][e] - dl));
+          dsb[kt][e >> 3][e & 7] = (__bf16)(p * (dp[kt][e] + ndl));
         }
       __builtin_amdgcn_sched_barrier(0);
       // dQ^T += K^T dS^T: K^T tile kt, half hh covers keys 32kt + 16hh + {4g+0..3, 8+4g+0..3}
@@ -269,13 +273,13 @@ __global__ __launch_bounds__(64 * (BLOCK / 32), (BLOCK == 128 || D == 64) ? 2 : 
 template <int D, int BLOCK>
 __global__ __launch_bounds__(128 * (BLOCK / 32), 1) void bwd_dkdv_kernel(
     const __bf16* __restrict__ Q, const __bf16* __restrict__ K, const __bf16* __restrict__ V,
-    const __bf16* __restrict__ dO, const float2* __restrict__ aux, __bf16* __restrict__ dK,
+    const __bf16* __restrict__ dO, const float* __restrict__ aux, __bf16* __restrict__ dK,
     __bf16* __restrict__ dV, int B, int N_all, int H, int nblk, float scale,
     const int32_t* __restrict__ colptr, const int32_t* __restrict__ rows_list,
     const int32_t* __restrict__ cu_seqlens, int64_t T_tok) {
   constexpr int NK = BLOCK / 32;        // key groups (waves per query half)
   using C = BwdCfg<D, BLOCK, 2 * NK>;
-  constexpr int AUXB = 1024;            // 64 rows x 8 bytes, padded to one load
+  constexpr int AUXB = 2048;            // 64 rows of each plane, one 1 KB load each
   __shared__ __attribute__((aligned(1024))) char q_lds0[C::TILEB];
   __shared__ __attribute__((aligned(1024))) char q_lds1[C::TILEB];
   __shared__ __attribute__((aligned(1024))) char o_lds0[C::TILEB];
@@ -342,9 +346,10 @@ __global__ __launch_bounds__(128 * (BLOCK / 32), 1) void bwd_dkdv_kernel(
         buffer_load_lds16(ro, od + (w * C::IPW + u) * 1024, lo.dma[u]);
       }
       if (w == 0) {   // rows past N (and lanes past the 64 rows) read zeros
-        const __amdgpu_buffer_rsrc_t ra =
-            buffer_rsrc(aux + sr.stat0 + r0, r0 < N ? min(N - r0, C::ST) * 8 : 0);
-        buffer_load_lds16(ra, ad, 16 * lane);
+        const int nb = r0 < N ? min(N - r0, C::ST) * 4 : 0;
+        buffer_load_lds16(buffer_rsrc(aux + sr.stat0 + r0, nb), ad, 16 * lane);
+        buffer_load_lds16(buffer_rsrc(aux + (int64_t)H * T_tok + sr.stat0 + r0, nb), ad + 1024,
+                          16 * lane);
       }
     };
     const float c2 = scale * kLog2e;
@@ -352,7 +357,14 @@ __global__ __launch_bounds__(128 * (BLOCK / 32), 1) void bwd_dkdv_kernel(
     auto step = [&](const char* qt_lds, const char* ot_lds, const char* at_lds)
         __attribute__((always_inline)) {
       // S = Q K^T and dP = dO V^T for this wave's 32 query rows (32 qh ..)
-      f32x16 s = f32x16{}, dp = f32x16{};
+      const float* const a_pl = reinterpret_cast<const float*>(at_lds) + 32 * qh + 4 * g;
+      f32x16 s = f32x16{}, dp;
+#pragma unroll
+      for (int a = 0; a < 4; ++a) {   // dP - delta directly: start at -delta
+        const f32x4 x = *reinterpret_cast<const f32x4*>(a_pl + 256 + 8 * a);
+#pragma unroll
+        for (int e = 0; e < 4; ++e) dp[4 * a + e] = x[e];
+      }
 #pragma unroll
       for (int ks = 0; ks < C::KS; ++ks) {
         const int off = lo.row[ks] + 32 * qh * C::ROWB;
@@ -365,17 +377,13 @@ __global__ __launch_bounds__(128 * (BLOCK / 32), 1) void bwd_dkdv_kernel(
       bf16x8 pb[2], dsb[2];
 #pragma unroll
       for (int a = 0; a < 4; ++a) {
-        const float* ap = reinterpret_cast<const float*>(at_lds) + 2 * (32 * qh + 8 * a + 4 * g);
-        const f32x4 x0 = *reinterpret_cast<const f32x4*>(ap);       // rows +0, +1
-        const f32x4 x1 = *reinterpret_cast<const f32x4*>(ap + 4);   // rows +2, +3
-        const float ls[4] = {x0[0], x0[2], x1[0], x1[2]};
-        const float dl[4] = {x0[1], x0[3], x1[1], x1[3]};
+        const f32x4 ls = *reinterpret_cast<const f32x4*>(a_pl + 8 * a);
 #pragma unroll
         for (int e = 0; e < 4; ++e) {
           const int idx = 4 * a + e;
           const float p = fast_exp2(__builtin_fmaf(s[idx], c2, -ls[e]));
           pb[idx >> 3][idx & 7] = (__bf16)p;
-          dsb[idx >> 3][idx & 7] = (__bf16)(p * (dp[idx] - dl[e]));
+          dsb[idx >> 3][idx & 7] = (__bf16)(p * dp[idx]);
         }
       }
       // dV^T += dO^T P and dK^T += Q^T dS over this wave's 32 query rows
@@ -466,7 +474,7 @@ hipError_t launch_bwd_t(const void* q, const void* k, const void* v, const void*
                         const AttnShape& sh, const int32_t* rowptr, const int32_t* cols,
                         const int32_t* colptr, const int32_t* rows, float* ws, hipStream_t s) {
   auto bf = [](const void* p) { return static_cast<const __bf16*>(p); };
-  float2* aux = reinterpret_cast<float2*>(ws);
+  float* aux = ws;
   const int64_t rows_total = sh.T * sh.H * (D / 8);
   hipLaunchKernelGGL((bwd_prep_kernel<D>), dim3((unsigned)((rows_total + 255) / 256)), dim3(256), 0,
                      s, bf(o), bf(dout), lse, aux, sh.T, sh.N, sh.H, sh.cu != nullptr);
