@@ -21,9 +21,11 @@
 //  * the loop is unrolled by two so that both LDS stages are at constant
 //    offsets: every LDS read address is a precomputed lane offset plus an
 //    immediate;
-//  * the running row max only moves when a new score exceeds it by more
-//    than 2^8 (log2 units), so the O rescale is rare (O and the row sum always
-//    use the same max, so the result is exact in real arithmetic);
+//  * no row max per tile: the exponentials use the running max set on the
+//    first tile, and a new max is taken (O and the row sum rescaled, the tile
+//    recomputed) only when a lane's tile sum exceeds 2^64 or is not finite,
+//    which keeps every value far inside fp32 range. O and the row sum always
+//    use the same max, so the result is exact in real arithmetic;
 //  * only the sub-tiles of a short last key block run the masking code.
 #include <type_traits>
 
@@ -35,7 +37,7 @@ namespace {
 
 constexpr float kLog2e = 1.4426950408889634f;
 constexpr float kLn2 = 0.6931471805599453f;
-constexpr float kRescaleSlack = 8.0f;   // log2 units: p = 2^(s - m) stays <= 256
+constexpr float kSumGuard = 18446744073709551616.0f;   // 2^64: per-lane tile sum bound
 
 template <int D, int BLOCK>
 struct FwdCfg {
@@ -179,31 +181,43 @@ __global__ __launch_bounds__(64 * (BLOCK / 32), (BLOCK == 128 || D == 64) ? 2 : 
         for (int e = 0; e < 16; ++e)
           s[kt][e] = 32 * kt + 8 * (e >> 2) + 4 * g + (e & 3) >= lim ? -INFINITY : s[kt][e];
     }
-    float mx = s[0][0];
-#pragma unroll
-    for (int kt = 0; kt < 2; ++kt)
-#pragma unroll
-      for (int e = (kt == 0 ? 1 : 0); e < 16; ++e) mx = fmaxf(mx, s[kt][e]);
-    mx = pair_max(mx) * c2;
-    if (__ballot(mx > m_run + kRescaleSlack)) {      // rare after the first tile
-      const float m_new = fmaxf(m_run, mx);
-      const float alpha = fast_exp2(m_run - m_new);  // 0 on the first tile
-      l_run *= alpha;
-#pragma unroll
-      for (int dt = 0; dt < C::DT; ++dt) oacc[dt] *= alpha;
-      m_run = m_new;
-    }
-    const float m_use = m_run == -INFINITY ? 0.f : m_run;
+    // Exponentials against the running max; the max itself is taken only on
+    // the first tile or when a tile's sum leaves the guard (rare).
     bf16x8 pb[2][2];
     float lsum = 0.f;
+    auto expo = [&]() __attribute__((always_inline)) {
+      const float m_use = m_run == -INFINITY ? 0.f : m_run;
+      lsum = 0.f;
 #pragma unroll
-    for (int kt = 0; kt < 2; ++kt)
+      for (int kt = 0; kt < 2; ++kt)
 #pragma unroll
-      for (int e = 0; e < 16; ++e) {
-        const float p = fast_exp2(__builtin_fmaf(s[kt][e], c2, -m_use));
-        lsum += p;
-        pb[kt][e >> 3][e & 7] = (__bf16)p;
+        for (int e = 0; e < 16; ++e) {
+          const float p = fast_exp2(__builtin_fmaf(s[kt][e], c2, -m_use));
+          lsum += p;
+          pb[kt][e >> 3][e & 7] = (__bf16)p;
+        }
+    };
+    bool redo = __ballot(m_run == -INFINITY) != 0;
+    if (!redo) {
+      expo();
+      redo = __ballot(!(lsum <= kSumGuard)) != 0;   // also catches inf and NaN
+    }
+    if (redo) {
+      float mx = s[0][0];
+#pragma unroll
+      for (int kt = 0; kt < 2; ++kt)
+#pragma unroll
+        for (int e = (kt == 0 ? 1 : 0); e < 16; ++e) mx = fmaxf(mx, s[kt][e]);
+      mx = pair_max(mx) * c2;
+      if (mx > m_run) {
+        const float alpha = fast_exp2(m_run - mx);   // 0 on the first tile
+        l_run *= alpha;
+#pragma unroll
+        for (int dt = 0; dt < C::DT; ++dt) oacc[dt] *= alpha;
+        m_run = mx;
       }
+      expo();
+    }
     l_run += lsum;
     // O^T += V^T P^T: P^T tile kt, half hh covers keys 32kt + 16hh + {4g+0..3, 8+4g+0..3}
 #pragma unroll

@@ -77,6 +77,23 @@ def test_peaky_scores_online_rescaling():
     check_grad(g["dv"], dV, "peaky dv")
 
 
+@pytest.mark.parametrize("seed,boost", [(13, 60.0), (14, 400.0)])
+def test_later_key_block_far_above_first_tile_max(seed, boost):
+    """Keys of the last block aligned with the queries make later tiles score
+    far above the first tile's maximum (2^(thousands) in log2 units for the
+    larger boost): the forward must take a new max and rescale rather than
+    overflow."""
+    case = W.random_case(seed, 900, 2, 128, 128, 0.6)
+    q = case["q"].float() * 4
+    k = case["k"].float().clone()
+    k[0, -200:] = q[0, :200] / q[0, :200].norm(dim=-1, keepdim=True) * boost
+    case["q"], case["k"] = q.to(torch.bfloat16), k.to(torch.bfloat16)
+    g = run_gpu(case, backward=False)
+    O, L = oracle.bsattn_fwd(case["q"], case["k"], case["v"], case["block_mask"], 128, case["scale"])
+    assert torch.isfinite(g["o"]).all() and torch.isfinite(g["lse"]).all()
+    check_out(g["o"], g["lse"], O, L, f"boost {boost}")
+
+
 def test_unit_values_give_unit_outputs_and_determinism():
     case = W.random_case(12, 1100, 3, 128, 128, 0.3)
     case["v"] = torch.ones_like(case["v"])
