@@ -215,6 +215,81 @@ def time_decode_prep(ut, fg_mask, grid: int, dev, stream, C: int = 64) -> dict:
     return out
 
 
+def time_varlen(ut, W, dev, stream, count: int = 8, reps: int = 10) -> dict:
+    """Packed samples of differing lengths: one foreground-count bucket of the
+    512-canvas workload (count samples, 24 heads x 128, block 128, block mask
+    density 0.3 + diagonal per sample), forward + backward through the
+    variable-length calls, against the same samples one uniform call each."""
+    import numpy as np
+    import torch
+    wl = W.WORKLOADS["c512"]
+    lens = W.bucket_lengths(wl.seed + 100, wl, count)
+    H, D, blk = wl.heads, wl.head_dim, wl.block
+    T, maxlen = sum(lens), max(lens)
+    nb = -(-maxlen // blk)
+    rng = np.random.default_rng(wl.seed + 101)
+    bm = (rng.random((count, H, nb, nb)) < 0.3).astype(np.uint8)
+    flops = 0
+    for b, n in enumerate(lens):
+        own = -(-n // blk)
+        bm[b, :, own:, :] = 0
+        bm[b, :, :, own:] = 0
+        d = np.arange(own)
+        bm[b][:, d, d] = 1
+        flops += W.retained_flops_fwd(bm[b:b + 1, :, :own, :own], n, blk, D)
+    g = torch.Generator(device=dev)
+    g.manual_seed(wl.seed + 102)
+    q, k, v, do = (torch.randn((T, H, D), generator=g, device=dev).to(torch.bfloat16) for _ in range(4))
+    cu = torch.tensor(np.concatenate([[0], np.cumsum(lens)]), dtype=torch.int32, device=dev)
+    sc = 1.0 / math.sqrt(D)
+    with torch.cuda.stream(stream):
+        idx = ut.build_block_index(torch.from_numpy(bm).to(dev))
+        o, lse = torch.empty_like(q), torch.empty((H, T), dtype=torch.float32, device=dev)
+        dq, dk, dv = torch.empty_like(q), torch.empty_like(q), torch.empty_like(q)
+        ws = torch.empty(ut.ut_bsattn_bwd_varlen_workspace_size(T, H), dtype=torch.uint8, device=dev)
+
+        def packed():
+            st = ut.ut_bsattn_fwd_varlen(q, k, v, o, lse, cu, maxlen, blk, idx["q_rowptr"],
+                                         idx["q_cols"], sc)
+            st |= ut.ut_bsattn_bwd_varlen(q, k, v, o, do, lse, dq, dk, dv, cu, maxlen, blk,
+                                          idx["q_rowptr"], idx["q_cols"], idx["kv_colptr"],
+                                          idx["kv_rows"], sc, ws)
+            if st != ut.UT_OK:
+                raise ut.UltraTexError("ut_bsattn_*_varlen", st, ut.last_error())
+
+        # the same samples, one uniform launch pair each
+        per = []
+        for b, n in enumerate(lens):
+            own = -(-n // blk)
+            t0 = int(cu[b])
+            sl = lambda x: x[t0:t0 + n].view(1, n, H, D)
+            per.append((sl(q), sl(k), sl(v), sl(do), n,
+                        ut.build_block_index(torch.from_numpy(np.ascontiguousarray(bm[b:b + 1, :, :own, :own])).to(dev))))
+        outs = [(torch.empty_like(a[0]), torch.empty((1, H, a[4]), dtype=torch.float32, device=dev),
+                 torch.empty_like(a[0]), torch.empty_like(a[0]), torch.empty_like(a[0])) for a in per]
+
+        def one_by_one():
+            for (qb, kb, vb, dob, n, ib), (ob, lb, dqb, dkb, dvb) in zip(per, outs):
+                st = ut.ut_bsattn_fwd(qb, kb, vb, ob, lb, blk, ib["q_rowptr"], ib["q_cols"], sc)
+                st |= ut.ut_bsattn_bwd(qb, kb, vb, ob, dob, lb, dqb, dkb, dvb, blk, ib["q_rowptr"],
+                                       ib["q_cols"], ib["kv_colptr"], ib["kv_rows"], sc, ws)
+                if st != ut.UT_OK:
+                    raise ut.UltraTexError("ut_bsattn_*", st, ut.last_error())
+
+        packed(); one_by_one()
+        torch.cuda.synchronize()
+        ms_packed = _time(packed, stream, reps)
+        ms_loop = _time(one_by_one, stream, reps)
+    tot = 3.5 * flops
+    return {"workload": f"{count} samples of one 512-canvas foreground-count bucket, 24 heads x 128, "
+                        f"block 128, density 0.3 + diagonal",
+            "lens": lens, "tokens": T, "fwd_flops": flops,
+            "ms_fwd_bwd_packed": round(ms_packed, 4),
+            "tflops_packed": round(tot / (ms_packed * 1e-3) / 1e12, 2),
+            "ms_fwd_bwd_one_by_one": round(ms_loop, 4),
+            "tflops_one_by_one": round(tot / (ms_loop * 1e-3) / 1e12, 2)}
+
+
 def main():
     args = parse()
     if args.gpus != 1:
@@ -351,6 +426,7 @@ def main():
     result["topk_mask"] = time_topk(ut, q, k, blk, W.kept_off_diagonal(wl.rho, nb), stream)
     result["fg_step"] = time_fg_step(ut, inst.fg_mask, wl.grid, dev, stream)
     result["decode_prep"] = time_decode_prep(ut, inst.fg_mask, wl.grid, dev, stream)
+    result["varlen"] = time_varlen(ut, W, dev, stream)
     if not args.no_cpu_baseline:
         result["cpu_baseline"] = cpu_baseline(inst, args.cpu_seconds)
     print(json.dumps(result), flush=True)
