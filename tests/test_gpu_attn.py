@@ -41,6 +41,10 @@ SMALL = [  # seed, N, H, D, block, density, batch, empty_rows
     (6, 512, 2, 128, 128, 0.5, 2, 0),     # exact multiple, batch 2
     (7, 1000, 2, 128, 128, 0.2, 1, 3),    # several empty rows
     (8, 1300, 4, 128, 128, 1.0, 1, 0),    # dense (all ones)
+    (9, 1, 2, 128, 128, 1.0, 1, 0),       # a single token
+    (10, 129, 2, 128, 128, 0.5, 1, 0),    # last block of one token
+    (11, 65, 2, 64, 64, 1.0, 1, 0),       # the same at block 64
+    (12, 64, 1, 64, 64, 1.0, 3, 0),       # one full block, batch 3
 ]
 
 
