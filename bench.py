@@ -373,8 +373,9 @@ def main():
         step(events[s])
     torch.cuda.synchronize()
     wall = time.perf_counter() - t0
-    per = {p: float(np.mean([events[s][i].elapsed_time(events[s][i + 1]) for s in range(args.steps)]))
-           for i, p in enumerate(phases)}
+    samples = {p: [events[s][i].elapsed_time(events[s][i + 1]) for s in range(args.steps)]
+               for i, p in enumerate(phases)}
+    per = {p: float(np.mean(x)) for p, x in samples.items()}
     ms_step = wall * 1e3 / args.steps
 
     fwd_flops = W.retained_flops_fwd(inst.block_mask, n, blk, D)
@@ -415,6 +416,8 @@ def main():
             "fwd_flops": fwd_flops,
         },
         "phases_ms": {p: round(per[p], 4) for p in phases},
+        "phases_ms_median": {p: round(float(np.median(samples[p])), 4) for p in phases},
+        "phases_ms_min": {p: round(float(np.min(samples[p])), 4) for p in phases},
         "copy": {"bytes_gather": copy_bytes,
                  "gbs_gather": round(copy_bytes / (per["drop"] * 1e-3) / 1e9, 1) if copy_bytes else None,
                  "gbs_scatter": round(copy_bytes / (per["scatter"] * 1e-3) / 1e9, 1) if copy_bytes else None},
