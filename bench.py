@@ -65,6 +65,9 @@ def parse():
     ap.add_argument("--workload", default="c2k_train")
     ap.add_argument("--rho", default="0.1")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    # the packed-sample timing launches the step's attention kernels again at
+    # other shapes; leave it out when a kernel trace should hold the step's only
+    ap.add_argument("--no-varlen", action="store_true")
     ap.add_argument("--cpu-seconds", type=float, default=12.0,
                     help="CPU time budget of the oracle baseline sample")
     return ap.parse_args()
@@ -429,7 +432,8 @@ def main():
     result["topk_mask"] = time_topk(ut, q, k, blk, W.kept_off_diagonal(wl.rho, nb), stream)
     result["fg_step"] = time_fg_step(ut, inst.fg_mask, wl.grid, dev, stream)
     result["decode_prep"] = time_decode_prep(ut, inst.fg_mask, wl.grid, dev, stream)
-    result["varlen"] = time_varlen(ut, W, dev, stream)
+    if not args.no_varlen:
+        result["varlen"] = time_varlen(ut, W, dev, stream)
     if not args.no_cpu_baseline:
         result["cpu_baseline"] = cpu_baseline(inst, args.cpu_seconds)
     print(json.dumps(result), flush=True)
