@@ -381,6 +381,10 @@ def main():
     per = {p: float(np.mean(x)) for p, x in samples.items()}
     ms_step = wall * 1e3 / args.steps
 
+    # the compaction alone (no rows), so that the gather's own rate can be
+    # separated from the drop phase
+    ms_compact = _time(lambda: check(ut.ut_drop_background(mask, None, None, kept, None, n_dev,
+                                                           ws_drop)[0], "drop"), stream)
     fwd_flops = W.retained_flops_fwd(inst.block_mask, n, blk, D)
     attn_flops = 3.5 * fwd_flops
     fwd_tflops = fwd_flops / (per["fwd"] * 1e-3) / 1e12
@@ -423,6 +427,9 @@ def main():
         "phases_ms_min": {p: round(float(np.min(samples[p])), 4) for p in phases},
         "copy": {"bytes_gather": copy_bytes,
                  "gbs_gather": round(copy_bytes / (per["drop"] * 1e-3) / 1e9, 1) if copy_bytes else None,
+                 "ms_compaction_only": round(ms_compact, 4),
+                 "gbs_gather_rows": round(copy_bytes / ((per["drop"] - ms_compact) * 1e-3) / 1e9, 1)
+                 if copy_bytes and per["drop"] > ms_compact else None,
                  "gbs_scatter": round(copy_bytes / (per["scatter"] * 1e-3) / 1e9, 1) if copy_bytes else None},
         "roofline": {"bound": "mfma", "kernel": "bsattn_fwd_kernel<128,128>",
                      "achieved": round(fwd_tflops, 2), "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s",
