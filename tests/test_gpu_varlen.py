@@ -3,7 +3,8 @@ ut_bsattn_bwd_varlen) against the oracle's per-sample Eq. 8: ragged lengths
 (short last blocks, a sample shorter than one block, an empty sample, block
 mask entries past a sample's end that must be ignored), equal lengths against
 the uniform calls bit for bit, a bucket of the 512-canvas workload at full
-head count, tokens covered by no sample, and the validation of the offsets."""
+head count, two 2048-canvas samples at full size (sampled rows), tokens
+covered by no sample, and the validation of the offsets."""
 import numpy as np
 import pytest
 import torch
@@ -99,6 +100,43 @@ def test_bucket_of_512_canvas_samples_full_heads():
         dQ, _, _ = oracle.bsattn_bwd(*sample, case["do"][None, sl], bm[b:b + 1, :, :nb, :nb], blk, sc,
                                      q_blocks=qb)
         check_grad(dq[sl], dQ[0], f"bucket sample {b} dq", rows=rows)
+
+
+def test_two_2k_samples_full_size_sampled():
+    """Per-GPU batch 2 at the 2048 canvas: two samples of one foreground-count
+    bucket (~77K kept tokens each, 24 heads x 128, block 128, density 0.1 +
+    diagonal) packed in one launch pair. The oracle checks, per sample and on
+    two heads, the first, a middle and the short last query block (O, LSE,
+    dQ), and dK / dV of the last key block from every query block selecting it."""
+    wl = W.WORKLOADS["c2k_train"]
+    lens = W.bucket_lengths(21, wl, 2)
+    case = W.varlen_case_device(22, lens, wl.heads, wl.head_dim, wl.block, 0.1, DEV)
+    q, k, v, do = case["q"], case["k"], case["v"], case["do"]
+    cu_h, bm, blk, sc = case["cu_seqlens"], case["block_mask"], case["block"], case["scale"]
+    cu = torch.from_numpy(cu_h).to(DEV)
+    idx = ut.build_block_index(torch.from_numpy(bm).to(DEV))
+    o, lse = ut.bsattn_fwd_varlen(q, k, v, cu, case["max_seqlen"], idx, blk, sc)
+    dq, dk, dv = ut.bsattn_bwd_varlen(q, k, v, o, do, lse, cu, case["max_seqlen"], idx, blk, sc)
+    torch.cuda.synchronize()
+    heads = [5, 19]
+    ht = torch.tensor(heads, device=DEV)
+    for b, n in enumerate(lens):
+        t0, nb = int(cu_h[b]), -(-n // blk)
+        sl = slice(t0, t0 + n)
+        x = [t[sl].index_select(1, ht).unsqueeze(0).cpu() for t in (q, k, v, do)]
+        m = np.ascontiguousarray(bm[b:b + 1][:, heads, :nb, :nb])
+        qb = [0, nb // 2, nb - 1]
+        rows = block_rows(qb, blk, n)
+        O, L = oracle.bsattn_fwd(*x[:3], m, blk, sc, q_blocks=qb)
+        check_out(o[sl].index_select(1, ht)[rows], lse.index_select(0, ht)[:, sl][:, rows],
+                  O[0][rows], L[0][:, rows], f"2K sample {b}")
+        jb = nb - 1
+        need = sorted(set(qb) | set(np.flatnonzero(m[0, :, :, jb].any(axis=0)).tolist()))
+        dQ, dK, dV = oracle.bsattn_bwd(*x, m, blk, sc, q_blocks=need)
+        check_grad(dq[sl].index_select(1, ht), dQ[0], f"2K sample {b} dq", rows=rows)
+        krows = block_rows([jb], blk, n)
+        check_grad(dk[sl].index_select(1, ht), dK[0], f"2K sample {b} dk", rows=krows)
+        check_grad(dv[sl].index_select(1, ht), dV[0], f"2K sample {b} dv", rows=krows)
 
 
 def test_tokens_outside_every_sample_are_untouched():

@@ -252,6 +252,32 @@ def varlen_case(seed: int, lens, heads: int, head_dim: int, block: int, density:
             "scale": 1.0 / math.sqrt(head_dim)}
 
 
+def varlen_case_device(seed: int, lens, heads: int, head_dim: int, block: int, density: float,
+                       device) -> dict:
+    """`varlen_case` for sizes too large to draw on the host: Q/K/V/dO come
+    from a seeded torch generator on `device` (N(0, 1) in fp32, rounded to
+    bf16); the offsets and the block mask (entries past each sample's blocks
+    zero) come from numpy as in `varlen_case`."""
+    import torch
+    rng = np.random.default_rng(seed)
+    lens = [int(x) for x in lens]
+    cu = np.concatenate([[0], np.cumsum(lens)]).astype(np.int32)
+    T, nb = int(cu[-1]), max(1, -(-max(lens) // block))
+    bm = (rng.random((len(lens), heads, nb, nb)) < density).astype(np.uint8)
+    for b, n in enumerate(lens):
+        own = -(-n // block)
+        bm[b, :, own:, :] = 0
+        bm[b, :, :, own:] = 0
+        d = np.arange(own)
+        bm[b][:, d, d] = 1
+    g = torch.Generator(device=device)
+    g.manual_seed(seed)
+    q, k, v, do = (torch.randn((T, heads, head_dim), generator=g, device=device).to(torch.bfloat16)
+                   for _ in range(4))
+    return {"q": q, "k": k, "v": v, "do": do, "cu_seqlens": cu, "block_mask": bm, "lens": lens,
+            "max_seqlen": max(max(lens), 1), "block": block, "scale": 1.0 / math.sqrt(head_dim)}
+
+
 def bucket_lengths(seed: int, wl: Workload, count: int) -> list:
     """Kept-token counts of `count` samples of one foreground-count bucket of a
     workload: each sample's count is its own draw of the workload's foreground
