@@ -1,6 +1,7 @@
 """More attention checks through the C ABI: a diagonal-only mask, gradient
 invariants at a mid size and at the full 2K size, the opt-in block-list
-validation mode, and launches on a non-default stream."""
+validation mode, launches on a non-default stream, and seeded sweeps over
+random shapes (uniform and packed batches)."""
 import math
 
 import numpy as np
@@ -109,3 +110,61 @@ def test_non_default_stream_matches_default():
     s.synchronize()
     for a, b in ((o, o_ref), (lse, lse_ref), (dq, dq_ref), (dk, dk_ref), (dv, dv_ref)):
         assert torch.equal(a, b)
+
+
+def test_random_shape_sweep():
+    """Twenty seeded random configurations (length, heads, head_dim, block,
+    batch, density, forced-empty rows), forward and backward against the
+    oracle element by element."""
+    rng = np.random.default_rng(2024)
+    for case_no in range(20):
+        n = int(rng.integers(1, 2500))
+        H = int(rng.integers(1, 4))
+        D = int(rng.choice([64, 128]))
+        blk = int(rng.choice([64, 128]))
+        batch = int(rng.integers(1, 3))
+        dens = float(rng.uniform(0.05, 1.0))
+        nb = -(-n // blk)
+        empty = int(rng.integers(0, min(3, nb) + 1))
+        seed = int(rng.integers(1 << 30))
+        label = f"sweep {case_no}: n={n} H={H} D={D} block={blk} B={batch} density={dens:.2f} empty={empty}"
+        print(label, flush=True)
+        case = W.random_case(seed, n, H, D, blk, dens, batch=batch, empty_rows=empty)
+        q, k, v, do, idx, o, lse, dq, dk, dv = _run(case)
+        O, L = oracle.bsattn_fwd(case["q"], case["k"], case["v"], case["block_mask"], blk, case["scale"])
+        check_out(o, lse, O, L, label)
+        grads = oracle.bsattn_bwd(case["q"], case["k"], case["v"], case["do"], case["block_mask"], blk,
+                                  case["scale"])
+        for got, ref, nm in zip((dq, dk, dv), grads, ("dq", "dk", "dv")):
+            check_grad(got, ref, f"{label} {nm}")
+
+
+def test_random_varlen_sweep():
+    """Ten seeded random packed batches (1-5 samples of 0-1500 tokens, some
+    shorter than a block) against the oracle element by element."""
+    rng = np.random.default_rng(2025)
+    for case_no in range(10):
+        count = int(rng.integers(1, 6))
+        lens = [int(x) for x in rng.integers(0, 1500, size=count)]
+        if max(lens) == 0:
+            lens[0] = 1
+        H = int(rng.integers(1, 3))
+        D = int(rng.choice([64, 128]))
+        blk = int(rng.choice([64, 128]))
+        dens = float(rng.uniform(0.1, 0.9))
+        label = f"varlen sweep {case_no}: lens={lens} H={H} D={D} block={blk} density={dens:.2f}"
+        print(label, flush=True)
+        c = W.varlen_case(int(rng.integers(1 << 30)), lens, H, D, blk, dens)
+        q, k, v, do = (c[x].to(DEV) for x in ("q", "k", "v", "do"))
+        cu = torch.from_numpy(c["cu_seqlens"]).to(DEV)
+        idx = ut.build_block_index(torch.from_numpy(c["block_mask"]).to(DEV))
+        o, lse = ut.bsattn_fwd_varlen(q, k, v, cu, c["max_seqlen"], idx, blk, c["scale"])
+        g = ut.bsattn_bwd_varlen(q, k, v, o, do, lse, cu, c["max_seqlen"], idx, blk, c["scale"])
+        torch.cuda.synchronize()
+        O, L = oracle.bsattn_fwd_varlen(c["q"], c["k"], c["v"], c["cu_seqlens"], c["block_mask"], blk,
+                                        c["scale"])
+        check_out(o, lse, O, L, label)
+        grads = oracle.bsattn_bwd_varlen(c["q"], c["k"], c["v"], c["do"], c["cu_seqlens"],
+                                         c["block_mask"], blk, c["scale"])
+        for got, ref, nm in zip(g, grads, ("dq", "dk", "dv")):
+            check_grad(got, ref, f"{label} {nm}")
