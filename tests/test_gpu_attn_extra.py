@@ -168,3 +168,22 @@ def test_random_varlen_sweep():
                                          c["block_mask"], blk, c["scale"])
         for got, ref, nm in zip(g, grads, ("dq", "dk", "dv")):
             check_grad(got, ref, f"{label} {nm}")
+
+
+def test_lse_normalises_the_allowed_scores():
+    """For sampled query rows, exp(s - LSE) summed over the row's allowed keys
+    (scores exact in float64 from the bf16 inputs) is 1; |LSE error| <= 1e-3
+    bounds the deviation by about 1e-3."""
+    case = W.random_case(41, 3000, 2, 128, 128, 0.3, empty_rows=0)
+    q, k, v, do, idx, o, lse, *_ = _run(case)
+    Q, K = case["q"].double().numpy()[0], case["k"].double().numpy()[0]
+    bm, blk, sc = case["block_mask"][0], 128, case["scale"]
+    L = lse.double().cpu().numpy()[0]
+    rng = np.random.default_rng(41)
+    for h in range(2):
+        for r in rng.choice(3000, 40, replace=False):
+            keys = np.concatenate([np.arange(j * blk, min(3000, (j + 1) * blk))
+                                   for j in np.flatnonzero(bm[h, r // blk])])
+            s = Q[r, h] @ K[keys, h].T * sc
+            tot = np.exp(s - L[h, r]).sum()
+            assert abs(tot - 1.0) <= 2e-3, (h, r, tot)
