@@ -10,12 +10,13 @@
 //           S^T = K Q^T and dP^T = V dO^T (lane = query column),
 //           P = exp(S - LSE), dS^T = P^T o (dP^T - delta), dQ^T += K^T dS^T;
 //   dK/dV : one workgroup per (b, h, key block j), walking the query blocks
-//           that select j (column lists). Waves w and w + BLOCK/32 own the
-//           same 32 keys (K rows in registers, V rows in LDS) and split each 64-row
-//           query tile between them: S = Q K^T and dP = dO V^T (lane = key
-//           column; the dP accumulator starts at -delta, so it ends as
-//           dP - delta), dV^T += dO^T P and dK^T += Q^T dS with transposing
-//           LDS reads. The two partial sums meet once in LDS at the end.
+//           that select j (column lists) in 32-row query tiles. One wave per
+//           32 keys (K rows in registers, the key block's V rows in LDS):
+//           S = Q K^T and dP = dO V^T (lane = key column; the dP accumulator
+//           starts at -delta, so it ends as dP - delta), dV^T += dO^T P and
+//           dK^T += Q^T dS with transposing LDS reads. Two workgroups share a
+//           CU, so the two waves on each SIMD belong to different workgroups
+//           and never wait at the same barrier.
 //
 // The dQ pass recomputes S and dP instead of accumulating dQ with atomics
 // from the dK/dV pass. Tiles go from global memory straight into LDS with
@@ -68,14 +69,14 @@ __global__ __launch_bounds__(256) void bwd_prep_kernel(const __bf16* __restrict_
   }
 }
 
-template <int D, int BLOCK, int NWAVES>
+template <int D, int BLOCK, int NWAVES, int ST_ = 64>
 struct BwdCfg {
   static constexpr int NT = 64 * NWAVES;
-  static constexpr int ST = 64;                  // rows per streamed tile
+  static constexpr int ST = ST_;                 // rows per streamed tile
   static constexpr int SUBS = BLOCK / ST;        // tiles per block
   static constexpr int ROWB = D * 2;
   static constexpr int CPR = D / 8;
-  static constexpr int TILEB = ST * ROWB;        // one 64-row bf16 tile
+  static constexpr int TILEB = ST * ROWB;        // one ST-row bf16 tile
   static constexpr int RPI = 1024 / ROWB;        // rows per direct-load instruction
   static constexpr int IPW = TILEB / 1024 / NWAVES;
   static constexpr int KS = D / 16;
@@ -268,18 +269,19 @@ __global__ __launch_bounds__(64 * (BLOCK / 32), (BLOCK == 128 || D == 64) ? 2 : 
 }
 
 // ---------------------------------------------------------------------------
-// dK, dV: key-stationary over the column lists, two waves per 32 keys
+// dK, dV: key-stationary over the column lists, one wave per 32 keys
 // ---------------------------------------------------------------------------
 template <int D, int BLOCK>
-__global__ __launch_bounds__(128 * (BLOCK / 32), 1) void bwd_dkdv_kernel(
+__global__ __launch_bounds__(64 * (BLOCK / 32), 256 / BLOCK) void bwd_dkdv_kernel(
     const __bf16* __restrict__ Q, const __bf16* __restrict__ K, const __bf16* __restrict__ V,
     const __bf16* __restrict__ dO, const float* __restrict__ aux, __bf16* __restrict__ dK,
     __bf16* __restrict__ dV, int B, int N_all, int H, int nblk, float scale,
     const int32_t* __restrict__ colptr, const int32_t* __restrict__ rows_list,
     const int32_t* __restrict__ cu_seqlens, int64_t T_tok) {
-  constexpr int NK = BLOCK / 32;        // key groups (waves per query half)
-  using C = BwdCfg<D, BLOCK, 2 * NK>;
-  constexpr int AUXB = 2048;            // 64 rows of each plane, one 1 KB load each
+  constexpr int NK = BLOCK / 32;        // key groups (one wave each)
+  using C = BwdCfg<D, BLOCK, NK, 32>;
+  constexpr int AUXB = 2048;            // 32 rows of each plane, one 1 KB load each
+  // 68 KB at head_dim 128, block 128: two workgroups fit one CU's LDS
   __shared__ __attribute__((aligned(1024))) char q_lds0[C::TILEB];
   __shared__ __attribute__((aligned(1024))) char q_lds1[C::TILEB];
   __shared__ __attribute__((aligned(1024))) char o_lds0[C::TILEB];
@@ -291,7 +293,7 @@ __global__ __launch_bounds__(128 * (BLOCK / 32), 1) void bwd_dkdv_kernel(
 
   const int tid = threadIdx.x, lane = tid & 63;
   const int w = __builtin_amdgcn_readfirstlane(tid >> 6);
-  const int kw = w % NK, qh = w / NK;   // 32-key group, query half of each tile
+  const int kw = w;   // 32-key group
   const int l32 = lane & 31, g = lane >> 5;
   const int64_t lt = blockIdx.x;   // tile order: see the launcher
   const int j = (int)(lt % nblk);
@@ -333,7 +335,7 @@ __global__ __launch_bounds__(128 * (BLOCK / 32), 1) void bwd_dkdv_kernel(
     }
     const char* const vrow = vblk_lds + 32 * kw * C::ROWB;   // this wave's 32 keys
 
-    // Tile t: 64 query rows of Q and dO, and their {LSE log2 e, delta}.
+    // Tile t: 32 query rows of Q and dO, and their {LSE log2 e, -delta}.
     auto load_tile = [&](int t, char* qd, char* od, char* ad) __attribute__((always_inline)) {
       const int i = rows_list[p0 + t / C::SUBS];
       const int r0 = i * BLOCK + (t % C::SUBS) * C::ST;
@@ -345,7 +347,7 @@ __global__ __launch_bounds__(128 * (BLOCK / 32), 1) void bwd_dkdv_kernel(
         buffer_load_lds16(rq, qd + (w * C::IPW + u) * 1024, lo.dma[u]);
         buffer_load_lds16(ro, od + (w * C::IPW + u) * 1024, lo.dma[u]);
       }
-      if (w == 0) {   // rows past N (and lanes past the 64 rows) read zeros
+      if (w == 0) {   // rows past N (and lanes past the tile's rows) read zeros
         const int nb = r0 < N ? min(N - r0, C::ST) * 4 : 0;
         buffer_load_lds16(buffer_rsrc(aux + sr.stat0 + r0, nb), ad, 16 * lane);
         buffer_load_lds16(buffer_rsrc(aux + (int64_t)H * T_tok + sr.stat0 + r0, nb), ad + 1024,
@@ -356,8 +358,8 @@ __global__ __launch_bounds__(128 * (BLOCK / 32), 1) void bwd_dkdv_kernel(
 
     auto step = [&](const char* qt_lds, const char* ot_lds, const char* at_lds)
         __attribute__((always_inline)) {
-      // S = Q K^T and dP = dO V^T for this wave's 32 query rows (32 qh ..)
-      const float* const a_pl = reinterpret_cast<const float*>(at_lds) + 32 * qh + 4 * g;
+      // S = Q K^T and dP = dO V^T for the tile's 32 query rows
+      const float* const a_pl = reinterpret_cast<const float*>(at_lds) + 4 * g;
       f32x16 s = f32x16{}, dp;
 #pragma unroll
       for (int a = 0; a < 4; ++a) {   // dP - delta directly: start at -delta
@@ -367,12 +369,12 @@ __global__ __launch_bounds__(128 * (BLOCK / 32), 1) void bwd_dkdv_kernel(
       }
 #pragma unroll
       for (int ks = 0; ks < C::KS; ++ks) {
-        const int off = lo.row[ks] + 32 * qh * C::ROWB;
+        const int off = lo.row[ks];
         s = mfma32(*reinterpret_cast<const bf16x8*>(qt_lds + off), kop[ks], s);
         const bf16x8 vop = *reinterpret_cast<const bf16x8*>(vrow + lo.row[ks]);
         dp = mfma32(*reinterpret_cast<const bf16x8*>(ot_lds + off), vop, dp);
       }
-      // rows 32 qh + 8 a + 4 g + (0..3): P and dS, as the B operands of the
+      // rows 8 a + 4 g + (0..3): P and dS, as the B operands of the
       // second products (half hh: rows 16 hh + {4g+0..3, 8+4g+0..3})
       bf16x8 pb[2], dsb[2];
 #pragma unroll
@@ -386,12 +388,12 @@ __global__ __launch_bounds__(128 * (BLOCK / 32), 1) void bwd_dkdv_kernel(
           dsb[idx >> 3][idx & 7] = (__bf16)(p * dp[idx]);
         }
       }
-      // dV^T += dO^T P and dK^T += Q^T dS over this wave's 32 query rows
+      // dV^T += dO^T P and dK^T += Q^T dS over the tile's 32 query rows
 #pragma unroll
       for (int dt = 0; dt < C::DT; ++dt)
 #pragma unroll
         for (int hh = 0; hh < 2; ++hh) {
-          const int rb = (32 * qh + 16 * hh) * C::ROWB;
+          const int rb = 16 * hh * C::ROWB;
           const s16x4 o_lo = lds_read_tr16(ot_lds + rb + lo.tr[dt][0]);
           const s16x4 o_hi = lds_read_tr16(ot_lds + rb + lo.tr[dt][1]);
           const s16x4 q_lo = lds_read_tr16(qt_lds + rb + lo.tr[dt][0]);
@@ -423,10 +425,6 @@ __global__ __launch_bounds__(128 * (BLOCK / 32), 1) void bwd_dkdv_kernel(
     if (t < T) iter(t, I0{});
   }
 
-  // The two query halves meet: the second half's partial sums go through LDS
-  // (one 16 KB region per key group), the first half adds them and stores.
-  char* const region = kw == 0 ? q_lds0 : kw == 1 ? q_lds1 : kw == 2 ? o_lds0 : o_lds1;
-  f32x4* const part = reinterpret_cast<f32x4*>(region) + lane;
   auto store_out = [&](__bf16* X, const f32x16 (&acc)[C::DT], float mul) __attribute__((always_inline)) {
     if (key >= N) return;
     const int64_t off = base_bh + (int64_t)key * tok_stride;
@@ -440,32 +438,8 @@ __global__ __launch_bounds__(128 * (BLOCK / 32), 1) void bwd_dkdv_kernel(
         *reinterpret_cast<bf16x4*>(X + off + 32 * dt + 8 * e4 + 4 * g) = v4;
       }
   };
-  auto merge = [&](f32x16 (&acc)[C::DT]) __attribute__((always_inline)) {
-    if (qh == 1) {
-#pragma unroll
-      for (int dt = 0; dt < C::DT; ++dt)
-#pragma unroll
-        for (int e4 = 0; e4 < 4; ++e4)
-          part[(4 * dt + e4) * 64] = f32x4{acc[dt][4 * e4], acc[dt][4 * e4 + 1], acc[dt][4 * e4 + 2],
-                                           acc[dt][4 * e4 + 3]};
-    }
-    __syncthreads();
-    if (qh == 0) {
-#pragma unroll
-      for (int dt = 0; dt < C::DT; ++dt)
-#pragma unroll
-        for (int e4 = 0; e4 < 4; ++e4) {
-          const f32x4 x = part[(4 * dt + e4) * 64];
-#pragma unroll
-          for (int e = 0; e < 4; ++e) acc[dt][4 * e4 + e] += x[e];
-        }
-    }
-    __syncthreads();
-  };
-  merge(dkt);
-  if (qh == 0) store_out(dK, dkt, scale);
-  merge(dvt);
-  if (qh == 0) store_out(dV, dvt, 1.f);
+  store_out(dK, dkt, scale);
+  store_out(dV, dvt, 1.f);
 }
 
 template <int D, int BLOCK>
@@ -483,7 +457,7 @@ hipError_t launch_bwd_t(const void* q, const void* k, const void* v, const void*
   // V stay in the shared last-level cache) and a run of heavy blocks is spread
   // over every XCD.
   const dim3 grid((unsigned)((int64_t)sh.B * sh.H * sh.nblk));
-  hipLaunchKernelGGL((bwd_dkdv_kernel<D, BLOCK>), grid, dim3(128 * (BLOCK / 32)), 0, s,
+  hipLaunchKernelGGL((bwd_dkdv_kernel<D, BLOCK>), grid, dim3(64 * (BLOCK / 32)), 0, s,
                      bf(q), bf(k), bf(v), bf(dout), aux, static_cast<__bf16*>(dk),
                      static_cast<__bf16*>(dv), sh.B, sh.N, sh.H, sh.nblk, sh.scale, colptr, rows,
                      sh.cu, sh.T);
