@@ -38,7 +38,7 @@ CAL_COPY_BYTES = 1 << 28      # calibration copy: 256 MiB read + 256 MiB written
 # those sources makes the figure stale and `traffic` is then reported as null.
 FWD_TRAFFIC = {
     "workload": "c2k_train", "rho": "0.1",
-    "read_bytes": 43.381e9, "write_bytes": 0.487e9,
+    "read_bytes": 43.681e9, "write_bytes": 0.487e9,
     "sources": ("bsattn_fwd.hip", "attn_util.h"),
     "sha256": "28c95bcf8fadd0947a6220c824582081dd1d3be5630ae94c23cd8eada1808b33",
 }
@@ -435,6 +435,12 @@ def main():
                      "achieved": round(fwd_tflops, 2), "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s",
                      "frac": round(fwd_tflops / PEAK_BF16_TFLOPS, 4),
                      "traffic": fwd_traffic(wl.name, wl.rho)},
+        # the backward call as a whole (pre-pass, dK/dV and dQ kernels, which
+        # run 7 products per pair for the 5 counted), timed like the forward
+        "roofline_bwd": {"bound": "mfma", "kernels": "bwd_prep_kernel + bwd_dkdv_kernel<128,128> + "
+                                                     "bwd_dq_kernel<128,128>",
+                         "achieved": round(bwd_tflops, 2), "peak": PEAK_BF16_TFLOPS,
+                         "unit": "TFLOP/s", "frac": round(bwd_tflops / PEAK_BF16_TFLOPS, 4)},
     }
     result["topk_mask"] = time_topk(ut, q, k, blk, W.kept_off_diagonal(wl.rho, nb), stream)
     result["fg_step"] = time_fg_step(ut, inst.fg_mask, wl.grid, dev, stream)
