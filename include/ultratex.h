@@ -161,7 +161,8 @@ ut_status ut_build_block_index(const uint8_t* block_mask, int32_t B, int32_t H,
  * q_rowptr, q_cols  the row lists of ut_build_block_index for [B, H, Nq, Nq].
  *           Contents are trusted: each j must lie in [0, Nq).
  * softmax_scale  the score scale, 1/sqrt(D) in the paper.
- * Errors: unsupported D / block -> UT_ERR_UNSUPPORTED; N < 1, B or H < 1,
+ * Errors: unsupported D / block, or one sample's [N, H, D] bf16 tensor of
+ *         2 GiB or more -> UT_ERR_UNSUPPORTED; N < 1, B or H < 1,
  *         null or misaligned pointers, non-finite scale -> UT_ERR_INVALID_ARG.
  * ---------------------------------------------------------------------- */
 ut_status ut_bsattn_fwd(const void* q, const void* k, const void* v, void* o,

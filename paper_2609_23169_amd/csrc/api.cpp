@@ -45,6 +45,11 @@ ut_status check_attn_common(const char* fn, int32_t B, int32_t N, int32_t H, int
   const int64_t nblk = (N + block - 1) / block;
   if ((int64_t)B * H * nblk >= (int64_t)1 << 31 || (int64_t)B * N * H * D >= (int64_t)1 << 40)
     return fail(UT_ERR_INVALID_ARG, "%s: problem too large", fn);
+  // the kernels bound their tile loads with 32-bit buffer ranges over one
+  // sample's rows
+  if ((int64_t)N * H * D * 2 >= (int64_t)1 << 31)
+    return fail(UT_ERR_UNSUPPORTED, "%s: one sample's Q/K/V of %d x %d x %d bf16 reach 2 GiB", fn,
+                N, H, D);
   return UT_OK;
 }
 

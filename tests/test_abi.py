@@ -57,6 +57,8 @@ def _fwd(**kw):
     (dict(v=MISALIGNED), ut.UT_ERR_INVALID_ARG, "aligned"),
     (dict(cols=None), ut.UT_ERR_INVALID_ARG, "q_cols is NULL"),
     (dict(scale=float("nan")), ut.UT_ERR_INVALID_ARG, "finite"),
+    # one sample's tensor of 2 GiB: 131072 x 64 x 128 bf16 (32-bit load ranges)
+    (dict(N=131072, H=64), ut.UT_ERR_UNSUPPORTED, "2 GiB"),
 ])
 def test_fwd_rejects_bad_arguments(kw, status, msg):
     assert _fwd(**kw) == status
@@ -72,6 +74,10 @@ def test_bwd_rejects_missing_workspace():
     assert st == ut.UT_ERR_WORKSPACE
     args[2] = None
     assert lib.ut_bsattn_bwd(*args, FAKE, 1600, None) == ut.UT_ERR_INVALID_ARG
+    args[2] = FAKE
+    args[10], args[11] = 131072, 64   # N, H: one sample's tensor reaches 2 GiB
+    assert lib.ut_bsattn_bwd(*args, FAKE, 131072 * 64 * 8, None) == ut.UT_ERR_UNSUPPORTED
+    assert "2 GiB" in ut.last_error()
 
 
 def _fwd_varlen(**kw):
@@ -92,6 +98,7 @@ def _fwd_varlen(**kw):
     (dict(D=96), ut.UT_ERR_UNSUPPORTED, "head_dim"),
     (dict(q=None), ut.UT_ERR_INVALID_ARG, "q is NULL"),
     (dict(lse=MISALIGNED), ut.UT_ERR_INVALID_ARG, "aligned"),
+    (dict(maxlen=131072, H=64, T=131072), ut.UT_ERR_UNSUPPORTED, "2 GiB"),
 ])
 def test_fwd_varlen_rejects_bad_arguments(kw, status, msg):
     assert _fwd_varlen(**kw) == status
