@@ -41,7 +41,7 @@
 extern "C" {
 #endif
 
-#define UT_ABI_VERSION 1
+#define UT_ABI_VERSION 2
 
 typedef enum {
   UT_OK = 0,
@@ -135,13 +135,25 @@ ut_status ut_scatter_foreground(const void* x_packed, const int32_t* kept_idx,
  *            not written.
  * nnz_host   optional: if non-NULL the call waits, stores the number of
  *            nonzero mask entries, and returns UT_ERR_CAPACITY if > cap.
- * Errors: any of B, H, Nq, Nk < 1, B*H*max(Nq,Nk) >= 2^31, null pointers ->
- *         UT_ERR_INVALID_ARG.
+ * workspace  device scratch of ut_build_block_index_workspace_size(B, H, Nq,
+ *            Nk) bytes. That size is 0 for every shape: the per-row and
+ *            per-column counts are written straight into q_rowptr and
+ *            kv_colptr and scanned there in place, so the build needs no
+ *            memory beyond its outputs. NULL with workspace_bytes = 0 is
+ *            valid; the arguments keep the signature uniform with the other
+ *            calls that take scratch.
+ * Errors: any of B, H, Nq, Nk < 1, B*H > 65535, B*H*Nq*Nk >= 2^31 (the
+ *         offsets are int32), null or misaligned pointers, cap < 0 ->
+ *         UT_ERR_INVALID_ARG; workspace_bytes below the required size ->
+ *         UT_ERR_WORKSPACE.
  * ---------------------------------------------------------------------- */
+size_t ut_build_block_index_workspace_size(int32_t B, int32_t H, int32_t Nq,
+                                           int32_t Nk);
 ut_status ut_build_block_index(const uint8_t* block_mask, int32_t B, int32_t H,
                                int32_t Nq, int32_t Nk, int32_t* q_rowptr,
                                int32_t* q_cols, int32_t* kv_colptr,
                                int32_t* kv_rows, int64_t cap, int64_t* nnz_host,
+                               void* workspace, size_t workspace_bytes,
                                hipStream_t stream);
 
 /* ------------------------------------------------------------------------
@@ -160,10 +172,14 @@ ut_status ut_build_block_index(const uint8_t* block_mask, int32_t B, int32_t H,
  *           excluded, rows beyond N are neither computed nor stored).
  * q_rowptr, q_cols  the row lists of ut_build_block_index for [B, H, Nq, Nq].
  *           Contents are trusted: each j must lie in [0, Nq).
- * softmax_scale  the score scale, 1/sqrt(D) in the paper.
+ * softmax_scale  the score scale, 1/sqrt(D) in the paper; must be finite
+ *           and > 0 (the kernels track the running maximum of the scaled
+ *           scores, which a zero or negative scale would turn into a
+ *           minimum, and mask keys with -inf scores).
  * Errors: unsupported D / block, or one sample's [N, H, D] bf16 tensor of
  *         2 GiB or more -> UT_ERR_UNSUPPORTED; N < 1, B or H < 1,
- *         null or misaligned pointers, non-finite scale -> UT_ERR_INVALID_ARG.
+ *         null or misaligned pointers, a scale that is not finite and
+ *         positive -> UT_ERR_INVALID_ARG.
  * ---------------------------------------------------------------------- */
 ut_status ut_bsattn_fwd(const void* q, const void* k, const void* v, void* o,
                         float* lse, int32_t B, int32_t N, int32_t H, int32_t D,

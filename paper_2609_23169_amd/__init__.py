@@ -19,7 +19,9 @@ import os
 import torch
 
 HERE = os.path.dirname(os.path.abspath(__file__))
-LIB_PATH = os.path.join(HERE, "libultratex.so")
+# UT_LIBRARY selects another build of the same library (the sanitized host
+# build of _build.py); by default the in-tree libultratex.so.
+LIB_PATH = os.environ.get("UT_LIBRARY") or os.path.join(HERE, "libultratex.so")
 
 UT_OK, UT_ERR_INVALID_ARG, UT_ERR_UNSUPPORTED, UT_ERR_WORKSPACE, UT_ERR_CAPACITY, UT_ERR_HIP = range(6)
 UT_BF16, UT_F32 = 0, 1
@@ -30,7 +32,7 @@ STATUS_NAMES = ["UT_OK", "UT_ERR_INVALID_ARG", "UT_ERR_UNSUPPORTED", "UT_ERR_WOR
 EXPORTS = [
     "ut_last_error", "ut_abi_version",
     "ut_drop_background_workspace_size", "ut_drop_background",
-    "ut_scatter_foreground", "ut_build_block_index",
+    "ut_scatter_foreground", "ut_build_block_index_workspace_size", "ut_build_block_index",
     "ut_bsattn_fwd", "ut_bsattn_bwd_workspace_size", "ut_bsattn_bwd",
     "ut_bsattn_fwd_varlen", "ut_bsattn_bwd_varlen_workspace_size", "ut_bsattn_bwd_varlen",
     "ut_topk_block_mask_workspace_size", "ut_topk_block_mask",
@@ -53,7 +55,9 @@ _SIGS = {
     "ut_drop_background_workspace_size": (_sz, [_i64]),
     "ut_drop_background": (_c.c_int, [_vp, _i64, _vp, _i64, _vp, _i64, _vp, _vp, _vp, _vp, _vp, _sz, _vp]),
     "ut_scatter_foreground": (_c.c_int, [_vp, _vp, _i64, _i64, _vp, _vp]),
-    "ut_build_block_index": (_c.c_int, [_vp, _i32, _i32, _i32, _i32, _vp, _vp, _vp, _vp, _i64, _vp, _vp]),
+    "ut_build_block_index_workspace_size": (_sz, [_i32, _i32, _i32, _i32]),
+    "ut_build_block_index": (_c.c_int, [_vp, _i32, _i32, _i32, _i32, _vp, _vp, _vp, _vp, _i64, _vp, _vp, _sz,
+                                        _vp]),
     "ut_bsattn_fwd": (_c.c_int, [_vp, _vp, _vp, _vp, _vp, _i32, _i32, _i32, _i32, _i32, _vp, _vp, _f32, _vp]),
     "ut_bsattn_bwd_workspace_size": (_sz, [_i32, _i32, _i32]),
     "ut_bsattn_bwd": (_c.c_int, [_vp, _vp, _vp, _vp, _vp, _vp, _vp, _vp, _vp, _i32, _i32, _i32, _i32, _i32,
@@ -168,9 +172,14 @@ def ut_scatter_foreground(x_packed, kept_idx, n_kept: int, x_full, stream=None) 
                                        _stream(stream))
 
 
+def ut_build_block_index_workspace_size(B: int, H: int, Nq: int, Nk: int) -> int:
+    return int(lib().ut_build_block_index_workspace_size(B, H, Nq, Nk))
+
+
 def ut_build_block_index(block_mask, q_rowptr, q_cols, kv_colptr, kv_rows, nnz_host: bool = False,
-                         stream=None):
-    """Returns (status, nnz or None)."""
+                         workspace=None, stream=None):
+    """Returns (status, nnz or None). The build needs no scratch (its size
+    query returns 0), so `workspace` may stay None."""
     _need(block_mask.dtype == torch.uint8 and block_mask.dim() == 4, "block_mask uint8 [B,H,Nq,Nk]")
     B, H, Nq, Nk = block_mask.shape
     _need(q_rowptr.numel() >= B * H * Nq + 1 and kv_colptr.numel() >= B * H * Nk + 1,
@@ -179,9 +188,11 @@ def ut_build_block_index(block_mask, q_rowptr, q_cols, kv_colptr, kv_rows, nnz_h
     for t in (q_rowptr, q_cols, kv_colptr, kv_rows):
         _need(t.dtype == torch.int32, "index arrays must be int32")
     host = ctypes.c_int64(-1)
+    ws_bytes = _nbytes(workspace) if workspace is not None else 0
     st = lib().ut_build_block_index(_p(block_mask), B, H, Nq, Nk, _p(q_rowptr), _p(q_cols),
                                     _p(kv_colptr), _p(kv_rows), cap,
-                                    ctypes.byref(host) if nnz_host else None, _stream(stream))
+                                    ctypes.byref(host) if nnz_host else None, _p(workspace),
+                                    ws_bytes, _stream(stream))
     return st, (host.value if nnz_host else None)
 
 

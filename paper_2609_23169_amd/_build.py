@@ -2,6 +2,13 @@
 
 Every source is compiled on each call (objects under _build/ next to this
 file), then linked into paper_2609_23169_amd/libultratex.so.
+
+`python -m paper_2609_23169_amd._build --sanitize` (or UT_SANITIZE=1) also
+builds _build/sanitize/libultratex_sanitize.so: the same kernels, with the
+host side of the C ABI (api.cpp: validation, workspace sizing, validate mode)
+compiled by g++ under AddressSanitizer and UndefinedBehaviorSanitizer. It is
+for CPU runs of the host paths only (README.md gives the command); the GPU
+code is never built with a sanitizer.
 """
 from __future__ import annotations
 
@@ -44,7 +51,34 @@ def _compile(src: str) -> str:
     return obj
 
 
-def build(verbose: bool = False) -> str:
+GXX = os.environ.get("CXX_HOST", "g++")
+SAN = os.path.join(OBJ, "sanitize")
+SAN_OUT = os.path.join(SAN, "libultratex_sanitize.so")
+SAN_FLAGS = ["-fsanitize=address,undefined", "-fno-omit-frame-pointer", "-fno-sanitize-recover=all"]
+
+
+def build_sanitized(objs, verbose: bool = False) -> str:
+    """api.cpp through g++ with ASan + UBSan, linked with the HIP objects."""
+    os.makedirs(SAN, exist_ok=True)
+    api_obj = os.path.join(SAN, "api.o")
+    cmd = [GXX, "-std=c++17", "-O1", "-g", "-fPIC", "-Wall", *SAN_FLAGS,
+           "-D__HIP_PLATFORM_AMD__", "-I/opt/rocm/include", "-I", os.path.join(ROOT, "include"),
+           "-I", CSRC, "-c", os.path.join(CSRC, "api.cpp"), "-o", api_obj]
+    r = subprocess.run(cmd, capture_output=True, text=True)
+    if r.returncode != 0:
+        raise RuntimeError(f"g++ (sanitized api.cpp) failed:\n{r.stdout}{r.stderr}")
+    kernels = [o for o in objs if os.path.basename(o) != "api.o"]
+    cmd = [GXX, "-shared", *SAN_FLAGS, api_obj, *kernels, "-L/opt/rocm/lib", "-lamdhip64",
+           "-Wl,-rpath,/opt/rocm/lib", "-o", SAN_OUT]
+    r = subprocess.run(cmd, capture_output=True, text=True)
+    if r.returncode != 0:
+        raise RuntimeError(f"sanitized link failed:\n{r.stdout}{r.stderr}")
+    if verbose:
+        print(f"built {SAN_OUT}")
+    return SAN_OUT
+
+
+def build(verbose: bool = False, sanitize: bool = False) -> str:
     os.makedirs(OBJ, exist_ok=True)
     with cf.ThreadPoolExecutor(max_workers=min(8, len(SOURCES))) as ex:
         objs = list(ex.map(_compile, SOURCES))
@@ -56,8 +90,10 @@ def build(verbose: bool = False) -> str:
     os.replace(tmp, OUT)
     if verbose:
         print(f"built {OUT}")
+    if sanitize or os.environ.get("UT_SANITIZE", "0") not in ("", "0"):
+        build_sanitized(objs, verbose)
     return OUT
 
 
 if __name__ == "__main__":
-    build(verbose=True)
+    build(verbose=True, sanitize="--sanitize" in sys.argv)

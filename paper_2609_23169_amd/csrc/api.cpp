@@ -30,6 +30,47 @@ ut_status check_hip(hipError_t e, const char* what) {
   return fail(UT_ERR_HIP, "%s: %s", what, hipGetErrorString(e));
 }
 
+// ptr[0] = 0, ptr non-decreasing, ptr[rows] = the number of entries given, and
+// each row's entries strictly ascending in [0, limit).
+ut_status check_lists(const char* fn, const char* what, const int32_t* ptr, const int32_t* idx,
+                      int64_t n_idx, int64_t rows, int32_t limit) {
+  if (ptr[0] != 0)
+    return fail(UT_ERR_INVALID_ARG, "%s: %s: pointers start at %d, not 0", fn, what, ptr[0]);
+  for (int64_t r = 0; r < rows; ++r)
+    if (ptr[r + 1] < ptr[r])
+      return fail(UT_ERR_INVALID_ARG, "%s: %s: pointers decrease at row %lld", fn, what,
+                  (long long)r);
+  if (!idx) return UT_OK;   // pointers only
+  if (ptr[rows] != n_idx)
+    return fail(UT_ERR_INVALID_ARG, "%s: %s: pointers end at %d, not at the %lld entries", fn,
+                what, ptr[rows], (long long)n_idx);
+  for (int64_t r = 0; r < rows; ++r)
+    for (int64_t e = ptr[r]; e < ptr[r + 1]; ++e) {
+      if (idx[e] < 0 || idx[e] >= limit)
+        return fail(UT_ERR_INVALID_ARG, "%s: %s: row %lld holds %d, outside [0, %d)", fn, what,
+                    (long long)r, idx[e], limit);
+      if (e > ptr[r] && idx[e] <= idx[e - 1])
+        return fail(UT_ERR_INVALID_ARG, "%s: %s: row %lld is not strictly ascending", fn, what,
+                    (long long)r);
+    }
+  return UT_OK;
+}
+
+ut_status check_cu_seqlens(const char* fn, const int32_t* cu, int32_t B, int64_t T,
+                           int32_t max_seqlen) {
+  if (cu[0] != 0 || cu[B] != T)
+    return fail(UT_ERR_INVALID_ARG, "%s: cu_seqlens must run from 0 to T = %lld (got %d .. %d)",
+                fn, (long long)T, cu[0], cu[B]);
+  for (int32_t b = 0; b < B; ++b) {
+    if (cu[b + 1] < cu[b])
+      return fail(UT_ERR_INVALID_ARG, "%s: cu_seqlens decreases at sample %d", fn, b);
+    if (cu[b + 1] - cu[b] > max_seqlen)
+      return fail(UT_ERR_INVALID_ARG, "%s: sample %d has %d tokens > max_seqlen %d", fn, b,
+                  cu[b + 1] - cu[b], max_seqlen);
+  }
+  return UT_OK;
+}
+
 namespace {
 
 ut_status check_attn_common(const char* fn, int32_t B, int32_t N, int32_t H, int32_t D,
@@ -40,8 +81,11 @@ ut_status check_attn_common(const char* fn, int32_t B, int32_t N, int32_t H, int
     return fail(UT_ERR_UNSUPPORTED, "%s: head_dim %d unsupported (64 or 128)", fn, D);
   if (block != 64 && block != 128)
     return fail(UT_ERR_UNSUPPORTED, "%s: block %d unsupported (64 or 128)", fn, block);
-  if (!std::isfinite(scale))
-    return fail(UT_ERR_INVALID_ARG, "%s: softmax_scale must be finite", fn);
+  // the kernels keep a running maximum of the scaled scores and mask keys with
+  // -inf scores; both need a positive scale
+  if (!std::isfinite(scale) || !(scale > 0.f))
+    return fail(UT_ERR_INVALID_ARG, "%s: softmax_scale must be finite and > 0 (got %g)", fn,
+                (double)scale);
   const int64_t nblk = (N + block - 1) / block;
   if ((int64_t)B * H * nblk >= (int64_t)1 << 31 || (int64_t)B * N * H * D >= (int64_t)1 << 40)
     return fail(UT_ERR_INVALID_ARG, "%s: problem too large", fn);
@@ -146,16 +190,28 @@ ut_status ut_scatter_foreground(const void* x_packed, const int32_t* kept_idx, i
                    "scatter launch");
 }
 
+size_t ut_build_block_index_workspace_size(int32_t B, int32_t H, int32_t Nq, int32_t Nk) {
+  // the counts are scanned in place inside q_rowptr / kv_colptr: no scratch
+  (void)B, (void)H, (void)Nq, (void)Nk;
+  return 0;
+}
+
 ut_status ut_build_block_index(const uint8_t* block_mask, int32_t B, int32_t H, int32_t Nq,
                                int32_t Nk, int32_t* q_rowptr, int32_t* q_cols,
                                int32_t* kv_colptr, int32_t* kv_rows, int64_t cap,
-                               int64_t* nnz_host, hipStream_t stream) {
+                               int64_t* nnz_host, void* workspace, size_t workspace_bytes,
+                               hipStream_t stream) {
   static const char* fn = "ut_build_block_index";
   g_last_error[0] = 0;
   if (B < 1 || H < 1 || Nq < 1 || Nk < 1)
     return fail(UT_ERR_INVALID_ARG, "%s: B, H, Nq, Nk must be >= 1", fn);
-  if ((int64_t)B * H > 65535 || (int64_t)B * H * (Nq > Nk ? Nq : Nk) >= ((int64_t)1 << 31))
-    return fail(UT_ERR_INVALID_ARG, "%s: problem too large", fn);
+  if ((int64_t)B * H > 65535)
+    return fail(UT_ERR_INVALID_ARG, "%s: B*H must be <= 65535 (got %lld)", fn,
+                (long long)B * H);
+  // list offsets are int32: the mask may not hold 2^31 entries
+  if ((int64_t)B * H * Nq * Nk >= ((int64_t)1 << 31))
+    return fail(UT_ERR_INVALID_ARG, "%s: B*H*Nq*Nk = %lld reaches 2^31 (int32 offsets)", fn,
+                (long long)B * H * Nq * Nk);
   if (cap < 0) return fail(UT_ERR_INVALID_ARG, "%s: cap < 0", fn);
   UT_TRY(check_ptr(fn, "block_mask", block_mask, 1));
   UT_TRY(check_ptr(fn, "q_rowptr", q_rowptr, 4));
@@ -164,6 +220,10 @@ ut_status ut_build_block_index(const uint8_t* block_mask, int32_t B, int32_t H, 
     UT_TRY(check_ptr(fn, "q_cols", q_cols, 4));
     UT_TRY(check_ptr(fn, "kv_rows", kv_rows, 4));
   }
+  const size_t need = ut_build_block_index_workspace_size(B, H, Nq, Nk);
+  if (workspace_bytes < need || (need > 0 && !workspace))
+    return fail(UT_ERR_WORKSPACE, "%s: workspace of %zu bytes required (got %zu)", fn, need,
+                workspace ? workspace_bytes : (size_t)0);
   UT_TRY(check_hip(launch_block_index(block_mask, B, H, Nq, Nk, q_rowptr, q_cols, kv_colptr,
                                       kv_rows, cap, stream),
                    "block index launch"));
@@ -174,7 +234,7 @@ ut_status ut_build_block_index(const uint8_t* block_mask, int32_t B, int32_t H, 
                      "nnz copy"));
     UT_TRY(check_hip(hipStreamSynchronize(stream), "stream sync"));
     *nnz_host = nnz;
-    if (nnz > cap)
+    if (nnz < 0 || nnz > cap)
       return fail(UT_ERR_CAPACITY, "%s: %d retained pairs exceed cap %lld", fn, nnz,
                   (long long)cap);
   }
@@ -189,8 +249,7 @@ bool validate_mode() {
   return e && e[0] && !(e[0] == '0' && e[1] == 0);
 }
 
-// Copies a compressed list pair to the host and checks it: ptr[0] = 0, ptr
-// non-decreasing, and each row's entries strictly ascending in [0, limit).
+// Copies a compressed list pair to the host and checks it with check_lists.
 ut_status validate_lists(const char* fn, const char* what, const int32_t* ptr, const int32_t* idx,
                          int64_t rows, int32_t limit, hipStream_t stream) {
   std::vector<int32_t> p((size_t)rows + 1);
@@ -198,11 +257,8 @@ ut_status validate_lists(const char* fn, const char* what, const int32_t* ptr, c
                                   stream),
                    "validate copy"));
   UT_TRY(check_hip(hipStreamSynchronize(stream), "validate sync"));
-  if (p[0] != 0) return fail(UT_ERR_INVALID_ARG, "%s: %s: pointers start at %d, not 0", fn, what, p[0]);
-  for (int64_t r = 0; r < rows; ++r)
-    if (p[r + 1] < p[r])
-      return fail(UT_ERR_INVALID_ARG, "%s: %s: pointers decrease at row %lld", fn, what,
-                  (long long)r);
+  // well-formed pointers first, so that p[rows] is a sane entry count
+  UT_TRY(check_lists(fn, what, p.data(), nullptr, 0, rows, limit));
   std::vector<int32_t> v((size_t)p[rows]);
   if (!v.empty()) {
     UT_TRY(check_hip(hipMemcpyAsync(v.data(), idx, v.size() * sizeof(int32_t),
@@ -210,16 +266,7 @@ ut_status validate_lists(const char* fn, const char* what, const int32_t* ptr, c
                      "validate copy"));
     UT_TRY(check_hip(hipStreamSynchronize(stream), "validate sync"));
   }
-  for (int64_t r = 0; r < rows; ++r)
-    for (int64_t e = p[r]; e < p[r + 1]; ++e) {
-      if (v[e] < 0 || v[e] >= limit)
-        return fail(UT_ERR_INVALID_ARG, "%s: %s: row %lld holds %d, outside [0, %d)", fn, what,
-                    (long long)r, v[e], limit);
-      if (e > p[r] && v[e] <= v[e - 1])
-        return fail(UT_ERR_INVALID_ARG, "%s: %s: row %lld is not strictly ascending", fn, what,
-                    (long long)r);
-    }
-  return UT_OK;
+  return check_lists(fn, what, p.data(), v.data(), (int64_t)v.size(), rows, limit);
 }
 }  // namespace
 
@@ -299,17 +346,7 @@ ut_status check_varlen(const char* fn, const int32_t* cu_seqlens, int32_t B, int
                                   hipMemcpyDeviceToHost, stream),
                    "validate copy"));
   UT_TRY(check_hip(hipStreamSynchronize(stream), "validate sync"));
-  if (cu[0] != 0 || cu[B] != T)
-    return fail(UT_ERR_INVALID_ARG, "%s: cu_seqlens must run from 0 to T = %lld (got %d .. %d)",
-                fn, (long long)T, cu[0], cu[B]);
-  for (int32_t b = 0; b < B; ++b) {
-    if (cu[b + 1] < cu[b])
-      return fail(UT_ERR_INVALID_ARG, "%s: cu_seqlens decreases at sample %d", fn, b);
-    if (cu[b + 1] - cu[b] > max_seqlen)
-      return fail(UT_ERR_INVALID_ARG, "%s: sample %d has %d tokens > max_seqlen %d", fn, b,
-                  cu[b + 1] - cu[b], max_seqlen);
-  }
-  return UT_OK;
+  return check_cu_seqlens(fn, cu.data(), B, T, max_seqlen);
 }
 }  // namespace
 

@@ -10,6 +10,8 @@
 //   2. an in-place scan of the counts into offsets (one workgroup per list);
 //   3. fill: the same traversals, each lane writing its index at
 //      offset + popcount of the set lanes below it.
+#include <hip/hip_runtime.h>
+
 #include "common.h"
 
 namespace ut {

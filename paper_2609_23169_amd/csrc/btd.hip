@@ -7,6 +7,8 @@
 // deterministic. The row copies are HBM-bound: one 64-lane wave moves one row
 // with 16-byte non-temporal loads and stores, all of a row's loads in flight
 // before its stores.
+#include <hip/hip_runtime.h>
+
 #include "common.h"
 
 namespace ut {
@@ -111,6 +113,7 @@ typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
 
 constexpr int kRowsPerBlock = kThreads / 64;  // one wave per row
 constexpr int kUnroll = 8;                    // 8 KiB of a row in flight per wave
+constexpr int64_t kGatherRowsPerPass = 131072;  // rows of one gather pass (32768 workgroups)
 
 __device__ inline void copy_row(const u32x4* __restrict__ s, u32x4* __restrict__ d, int64_t nvec) {
   const int lane = threadIdx.x & 63;
@@ -125,15 +128,21 @@ __device__ inline void copy_row(const u32x4* __restrict__ s, u32x4* __restrict__
   }
 }
 
+// The kept count is only known on the device, so the grid is sized for
+// min(capacity, kGatherRowsPerPass) rows and each wave strides over the kept
+// rows: a capacity far above the kept count launches no idle workgroups
+// beyond one pass.
 __global__ __launch_bounds__(kThreads) void gather_rows(const u32x4* __restrict__ src, int64_t nvec,
                                                         u32x4* __restrict__ dst, int64_t capacity,
                                                         const int32_t* __restrict__ kept_idx,
                                                         const int32_t* __restrict__ n_kept) {
   const int64_t n = min((int64_t)*n_kept, capacity);
-  const int64_t row = (int64_t)blockIdx.x * kRowsPerBlock + (threadIdx.x >> 6);
-  if (row >= n) return;
-  const int64_t srow = kept_idx[row];
-  copy_row(src + srow * nvec, dst + row * nvec, nvec);
+  const int64_t stride = (int64_t)gridDim.x * kRowsPerBlock;
+  for (int64_t row = (int64_t)blockIdx.x * kRowsPerBlock + (threadIdx.x >> 6); row < n;
+       row += stride) {
+    const int64_t srow = kept_idx[row];
+    copy_row(src + srow * nvec, dst + row * nvec, nvec);
+  }
 }
 
 __global__ __launch_bounds__(kThreads) void scatter_rows(const u32x4* __restrict__ src, int64_t nvec,
@@ -163,7 +172,8 @@ hipError_t launch_compact(const uint8_t* mask, int64_t L, int64_t capacity, int3
 hipError_t launch_gather(const void* x_full, int64_t row_bytes, void* x_packed, int64_t capacity,
                          const int32_t* kept_idx, const int32_t* n_kept, hipStream_t s) {
   if (capacity == 0) return hipSuccess;
-  const int64_t blocks = (capacity + kRowsPerBlock - 1) / kRowsPerBlock;
+  const int64_t rows = min(capacity, kGatherRowsPerPass);
+  const int64_t blocks = (rows + kRowsPerBlock - 1) / kRowsPerBlock;
   hipLaunchKernelGGL(gather_rows, dim3((unsigned)blocks), dim3(kThreads), 0, s,
                      static_cast<const u32x4*>(x_full), row_bytes / 16,
                      static_cast<u32x4*>(x_packed), capacity, kept_idx, n_kept);

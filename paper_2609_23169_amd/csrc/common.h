@@ -1,7 +1,9 @@
 // Internal declarations shared by the HIP sources of libultratex.so.
 #pragma once
 
-#include <hip/hip_runtime.h>
+// Host-side declarations only (api.cpp builds with a plain C++ compiler too);
+// the kernel sources include hip_runtime.h themselves.
+#include <hip/hip_runtime_api.h>
 #include <stdint.h>
 
 #include "ultratex.h"
@@ -12,6 +14,16 @@ namespace ut {
 ut_status fail(ut_status st, const char* fmt, ...);
 // Maps a HIP error (if any) to UT_ERR_HIP with context; UT_OK otherwise.
 ut_status check_hip(hipError_t e, const char* what);
+
+// Host checks of the validate mode, on host copies of the arguments.
+// Compressed lists: ptr[0] = 0, ptr non-decreasing, ptr[rows] = n_idx, and
+// every row strictly ascending within [0, limit). With idx = NULL only the
+// first two properties are checked.
+ut_status check_lists(const char* fn, const char* what, const int32_t* ptr, const int32_t* idx,
+                      int64_t n_idx, int64_t rows, int32_t limit);
+// Sample offsets: cu[0] = 0, cu[B] = T, non-decreasing, no sample > max_seqlen.
+ut_status check_cu_seqlens(const char* fn, const int32_t* cu, int32_t B, int64_t T,
+                           int32_t max_seqlen);
 
 // ---- Background Token Dropping (btd.hip) ----
 constexpr int kCompactTile = 4096;   // mask bytes per workgroup of the scan

@@ -11,6 +11,8 @@
 //               alpha > threshold); dilate: one thread per token ORs the
 //               (2 radius + 1)^2 square of pooled tokens around it, clipped
 //               at the view border.
+#include <hip/hip_runtime.h>
+
 #include "common.h"
 
 namespace ut {

@@ -14,6 +14,8 @@
 //           2 d / (n C) is written in fp32.
 // Entries of kept outside [0, L) are skipped (they would address memory
 // outside the grids).
+#include <hip/hip_runtime.h>
+
 #include "common.h"
 
 namespace ut {

@@ -21,6 +21,8 @@
 //            the k best blocks are chosen among the rest.
 #include <algorithm>
 
+#include <hip/hip_runtime.h>
+
 #include "common.h"
 
 namespace ut {

@@ -28,7 +28,7 @@ def test_library_exports_every_declared_symbol():
     lib = ut.lib()
     for name in declared_functions():
         assert hasattr(lib, name), name
-    assert lib.ut_abi_version() == 1
+    assert lib.ut_abi_version() == 2
 
 
 def test_workspace_sizes():
@@ -57,6 +57,8 @@ def _fwd(**kw):
     (dict(v=MISALIGNED), ut.UT_ERR_INVALID_ARG, "aligned"),
     (dict(cols=None), ut.UT_ERR_INVALID_ARG, "q_cols is NULL"),
     (dict(scale=float("nan")), ut.UT_ERR_INVALID_ARG, "finite"),
+    (dict(scale=0.0), ut.UT_ERR_INVALID_ARG, "> 0"),
+    (dict(scale=-0.088), ut.UT_ERR_INVALID_ARG, "> 0"),
     # one sample's tensor of 2 GiB: 131072 x 64 x 128 bf16 (32-bit load ranges)
     (dict(N=131072, H=64), ut.UT_ERR_UNSUPPORTED, "2 GiB"),
 ])
@@ -80,6 +82,17 @@ def test_bwd_rejects_missing_workspace():
     assert "2 GiB" in ut.last_error()
 
 
+def test_bwd_rejects_non_positive_scale():
+    lib = ut.lib()
+    for scale in (0.0, -0.088, float("inf")):
+        args = [FAKE] * 9 + [1, 100, 2, 128, 128] + [FAKE] * 4 + [scale]
+        assert lib.ut_bsattn_bwd(*args, FAKE, 1600, None) == ut.UT_ERR_INVALID_ARG
+        assert "softmax_scale" in ut.last_error()
+        vargs = [FAKE] * 10 + [3, 300, 128, 2, 128, 128] + [FAKE] * 4 + [scale]
+        assert lib.ut_bsattn_bwd_varlen(*vargs, FAKE, 4800, None) == ut.UT_ERR_INVALID_ARG
+        assert "softmax_scale" in ut.last_error()
+
+
 def _fwd_varlen(**kw):
     a = dict(q=FAKE, k=FAKE, v=FAKE, o=FAKE, lse=FAKE, cu=FAKE, B=3, T=300, maxlen=128, H=2, D=128,
              block=128, rowptr=FAKE, cols=FAKE, scale=0.1)
@@ -99,6 +112,8 @@ def _fwd_varlen(**kw):
     (dict(q=None), ut.UT_ERR_INVALID_ARG, "q is NULL"),
     (dict(lse=MISALIGNED), ut.UT_ERR_INVALID_ARG, "aligned"),
     (dict(maxlen=131072, H=64, T=131072), ut.UT_ERR_UNSUPPORTED, "2 GiB"),
+    (dict(scale=0.0), ut.UT_ERR_INVALID_ARG, "> 0"),
+    (dict(scale=-1.0), ut.UT_ERR_INVALID_ARG, "> 0"),
 ])
 def test_fwd_varlen_rejects_bad_arguments(kw, status, msg):
     assert _fwd_varlen(**kw) == status
@@ -148,12 +163,25 @@ def test_scatter_and_block_index_reject_bad_arguments():
     assert lib.ut_scatter_foreground(None, None, 0, 32, None, None) == ut.UT_OK   # no-op
     assert lib.ut_scatter_foreground(FAKE, FAKE, 10, 32, MISALIGNED, None) == ut.UT_ERR_INVALID_ARG
     bi = lambda B=1, H=2, Nq=5, Nk=5, mask=FAKE, rp=FAKE, cap=50: lib.ut_build_block_index(
-        mask, B, H, Nq, Nk, rp, FAKE, FAKE, FAKE, cap, None, None)
+        mask, B, H, Nq, Nk, rp, FAKE, FAKE, FAKE, cap, None, None, 0, None)
     assert bi(Nq=0) == ut.UT_ERR_INVALID_ARG
     assert bi(mask=None) == ut.UT_ERR_INVALID_ARG
     assert bi(rp=MISALIGNED) == ut.UT_ERR_INVALID_ARG
     assert bi(cap=-1) == ut.UT_ERR_INVALID_ARG
-    assert bi(B=300, H=300) == ut.UT_ERR_INVALID_ARG
+    assert bi(B=300, H=300) == ut.UT_ERR_INVALID_ARG and "65535" in ut.last_error()
+    # 2^31 mask entries would wrap the int32 list offsets
+    assert bi(B=1, H=2, Nq=32768, Nk=32768) == ut.UT_ERR_INVALID_ARG
+    assert "2^31" in ut.last_error()
+    assert bi(B=1, H=2, Nq=32768, Nk=32767, mask=None) == ut.UT_ERR_INVALID_ARG   # just below
+
+
+def test_block_index_needs_no_workspace():
+    for shape in ((1, 24, 603, 603), (1, 1, 1, 1), (2, 2, 70, 65)):
+        assert ut.ut_build_block_index_workspace_size(*shape) == 0
+    lib = ut.lib()
+    # a NULL workspace of 0 bytes passes the checks (a NULL mask is then the error)
+    st = lib.ut_build_block_index(None, 1, 2, 5, 5, FAKE, FAKE, FAKE, FAKE, 50, None, None, 0, None)
+    assert st == ut.UT_ERR_INVALID_ARG and "block_mask is NULL" in ut.last_error()
 
 
 def test_binding_refuses_host_tensors():

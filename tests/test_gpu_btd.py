@@ -41,7 +41,10 @@ def test_compaction_unaligned_mask_pointer():
 
 
 @pytest.mark.parametrize("L,row_elems,p", [(777, 8, 0.4), (5000, 24, 0.6), (4096, 3072, 0.35),
-                                           (33, 64, 1.0), (50, 64, 0.0)])
+                                           (33, 64, 1.0), (50, 64, 0.0),
+                                           # ~180K kept rows: more than one pass of the
+                                           # gather grid, so waves take several rows
+                                           (300000, 8, 0.6)])
 def test_gather_scatter_bit_exact(L, row_elems, p):
     rng = np.random.default_rng(L + row_elems)
     m = _mask(L, p, L)
