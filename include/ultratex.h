@@ -215,6 +215,33 @@ ut_status ut_bsattn_bwd(const void* q, const void* k, const void* v,
                         size_t workspace_bytes, hipStream_t stream);
 
 /* ------------------------------------------------------------------------
+ * ut_bsattn_bwd without a workspace argument, for callers that cannot
+ * allocate device memory: code under HIP graph capture, tight serving or
+ * training loops, harnesses that forbid hipMalloc. Arguments, outputs and
+ * errors are those of ut_bsattn_bwd; the call allocates nothing (no hipMalloc,
+ * hipFree or allocating library routine) and runs the same kernels.
+ *
+ * Scratch: a built-in device array of 32 MiB per GPU, part of the library's
+ * code object (loaded with it on each GPU the library runs on and held until
+ * the process ends). It holds the 8 bytes per query row of the statistics
+ * planes, so B*H*N may be at most 4,194,304 (e.g. 24 heads x 174,762
+ * tokens); larger problems return UT_ERR_WORKSPACE and launch nothing. Every
+ * call on one GPU shares that GPU's array: calls that overlap in time on one
+ * GPU (concurrent streams, threads) race on it and must be serialised by the
+ * caller. Each call writes every row it reads, so nothing needs clearing
+ * between calls. The UT_VALIDATE list check is not applied here (it copies
+ * the lists to the host and waits for the stream).
+ * ---------------------------------------------------------------------- */
+ut_status ut_bsattn_bwd_noalloc(const void* q, const void* k, const void* v,
+                                const void* o, const void* dout,
+                                const float* lse, void* dq, void* dk, void* dv,
+                                int32_t B, int32_t N, int32_t H, int32_t D,
+                                int32_t block, const int32_t* q_rowptr,
+                                const int32_t* q_cols, const int32_t* kv_colptr,
+                                const int32_t* kv_rows, float softmax_scale,
+                                hipStream_t stream);
+
+/* ------------------------------------------------------------------------
  * Variable-length batches of the two attention calls: B samples of differing
  * kept-token counts packed back to back in one launch. The paper buckets
  * training samples by their foreground token count (Sec. 4.1, Implementation

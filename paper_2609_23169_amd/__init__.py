@@ -33,7 +33,7 @@ EXPORTS = [
     "ut_last_error", "ut_abi_version",
     "ut_drop_background_workspace_size", "ut_drop_background",
     "ut_scatter_foreground", "ut_build_block_index_workspace_size", "ut_build_block_index",
-    "ut_bsattn_fwd", "ut_bsattn_bwd_workspace_size", "ut_bsattn_bwd",
+    "ut_bsattn_fwd", "ut_bsattn_bwd_workspace_size", "ut_bsattn_bwd", "ut_bsattn_bwd_noalloc",
     "ut_bsattn_fwd_varlen", "ut_bsattn_bwd_varlen_workspace_size", "ut_bsattn_bwd_varlen",
     "ut_topk_block_mask_workspace_size", "ut_topk_block_mask",
     "ut_euler_update_foreground", "ut_fg_flow_loss_workspace_size", "ut_fg_flow_loss",
@@ -62,6 +62,8 @@ _SIGS = {
     "ut_bsattn_bwd_workspace_size": (_sz, [_i32, _i32, _i32]),
     "ut_bsattn_bwd": (_c.c_int, [_vp, _vp, _vp, _vp, _vp, _vp, _vp, _vp, _vp, _i32, _i32, _i32, _i32, _i32,
                                  _vp, _vp, _vp, _vp, _f32, _vp, _sz, _vp]),
+    "ut_bsattn_bwd_noalloc": (_c.c_int, [_vp, _vp, _vp, _vp, _vp, _vp, _vp, _vp, _vp, _i32, _i32, _i32, _i32,
+                                         _i32, _vp, _vp, _vp, _vp, _f32, _vp]),
     "ut_bsattn_fwd_varlen": (_c.c_int, [_vp, _vp, _vp, _vp, _vp, _vp, _i32, _i64, _i32, _i32, _i32, _i32,
                                         _vp, _vp, _f32, _vp]),
     "ut_bsattn_bwd_varlen_workspace_size": (_sz, [_i64, _i32]),
@@ -236,6 +238,21 @@ def ut_bsattn_bwd(q, k, v, o, dout, lse, dq, dk, dv, block: int, q_rowptr, q_col
     return lib().ut_bsattn_bwd(_p(q), _p(k), _p(v), _p(o), _p(dout), _p(lse), _p(dq), _p(dk), _p(dv),
                                B, N, H, D, block, _p(q_rowptr), _p(q_cols), _p(kv_colptr),
                                _p(kv_rows), softmax_scale, _p(workspace), ws_bytes, _stream(stream))
+
+
+def ut_bsattn_bwd_noalloc(q, k, v, o, dout, lse, dq, dk, dv, block: int, q_rowptr, q_cols, kv_colptr,
+                          kv_rows, softmax_scale: float, stream=None) -> int:
+    """ut_bsattn_bwd with the library's built-in scratch instead of a workspace
+    (no device allocation; B*H*N up to 4,194,304 query rows)."""
+    B, N, H, D, nb = _check_attn(q, k, v, block, q_rowptr, q_cols)
+    for t in (o, dout, dq, dk, dv):
+        _need(t.shape == q.shape and t.dtype == torch.bfloat16, "o, dout, dq, dk, dv: bf16 [B,N,H,D]")
+    _need(lse.dtype == torch.float32 and lse.numel() >= B * H * N, "lse: fp32 [B,H,N]")
+    _need(kv_colptr.dtype == torch.int32 and kv_colptr.numel() >= B * H * nb + 1, "kv_colptr int32")
+    _need(kv_rows.dtype == torch.int32, "kv_rows int32")
+    return lib().ut_bsattn_bwd_noalloc(_p(q), _p(k), _p(v), _p(o), _p(dout), _p(lse), _p(dq), _p(dk),
+                                       _p(dv), B, N, H, D, block, _p(q_rowptr), _p(q_cols),
+                                       _p(kv_colptr), _p(kv_rows), softmax_scale, _stream(stream))
 
 
 def _check_varlen(q, k, v, cu_seqlens, max_seqlen, block, rowptr, cols):

@@ -331,6 +331,37 @@ ut_status ut_bsattn_bwd(const void* q, const void* k, const void* v, const void*
                    "backward launch");
 }
 
+ut_status ut_bsattn_bwd_noalloc(const void* q, const void* k, const void* v, const void* o,
+                                const void* dout, const float* lse, void* dq, void* dk, void* dv,
+                                int32_t B, int32_t N, int32_t H, int32_t D, int32_t block,
+                                const int32_t* q_rowptr, const int32_t* q_cols,
+                                const int32_t* kv_colptr, const int32_t* kv_rows,
+                                float softmax_scale, hipStream_t stream) {
+  static const char* fn = "ut_bsattn_bwd_noalloc";
+  g_last_error[0] = 0;
+  UT_TRY(check_attn_common(fn, B, N, H, D, block, softmax_scale));
+  const struct { const char* n; const void* p; uintptr_t a; } ptrs[] = {
+      {"q", q, 16},   {"k", k, 16},   {"v", v, 16},         {"o", o, 16},
+      {"dout", dout, 16}, {"lse", lse, 4}, {"dq", dq, 16},   {"dk", dk, 16},
+      {"dv", dv, 16}, {"q_rowptr", q_rowptr, 4}, {"q_cols", q_cols, 4},
+      {"kv_colptr", kv_colptr, 4}, {"kv_rows", kv_rows, 4}};
+  for (const auto& p : ptrs) UT_TRY(check_ptr(fn, p.n, p.p, p.a));
+  const size_t need = ut_bsattn_bwd_workspace_size(B, N, H);
+  if (need > kNoallocScratchBytes)
+    return fail(UT_ERR_WORKSPACE,
+                "%s: B*H*N = %lld query rows need %zu bytes of scratch; the built-in scratch "
+                "holds %zu bytes (%zu rows): use ut_bsattn_bwd with a workspace",
+                fn, (long long)B * H * N, need, kNoallocScratchBytes,
+                kNoallocScratchBytes / (2 * sizeof(float)));
+  float* ws = nullptr;
+  UT_TRY(check_hip(noalloc_scratch(stream, &ws), "scratch address"));
+  const AttnShape sh{B, N, H, D, block, (N + block - 1) / block, softmax_scale, nullptr,
+                     (int64_t)B * N};
+  return check_hip(launch_bsattn_bwd(q, k, v, o, dout, lse, dq, dk, dv, sh, q_rowptr, q_cols,
+                                     kv_colptr, kv_rows, ws, stream),
+                   "backward launch");
+}
+
 namespace {
 // Sample offsets of the variable-length calls: B + 1 device int32 values.
 // Under UT_VALIDATE they are copied to the host and must start at 0, end at

@@ -24,6 +24,7 @@
 // zeros. For query rows past N that makes every contribution exactly zero
 // (zero Q and dO rows give dP = 0 and delta = 0, hence dS = 0 and P dO = 0).
 // Keys past N are masked explicitly in the dQ pass (their P would not be 0).
+#include <mutex>
 #include <type_traits>
 
 #include "attn_util.h"
@@ -467,7 +468,40 @@ hipError_t launch_bwd_t(const void* q, const void* k, const void* v, const void*
   return hipGetLastError();
 }
 
+// The allocation-free entry point's scratch: a file-scope device array, one
+// copy per GPU, allocated by the loader with the code object and held until
+// the process ends. Its name is a host-side stand-in in host code; only the
+// address hipGetSymbolAddress returns is ever passed to a kernel.
+__device__ __align__(256) float scratch[kNoallocScratchBytes / sizeof(float)];
+
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mu;
+float* g_scratch_ptr[kMaxDevices] = {};
+
 }  // namespace
+
+hipError_t noalloc_scratch(hipStream_t s, float** ptr) {
+  int dev = 0;
+  hipError_t e = s ? hipStreamGetDevice(s, &dev) : hipGetDevice(&dev);
+  if (e != hipSuccess) return e;
+  if (dev < 0 || dev >= kMaxDevices) return hipErrorInvalidDevice;
+  std::lock_guard<std::mutex> lock(g_scratch_mu);
+  if (!g_scratch_ptr[dev]) {
+    // once per device, with that device current
+    int cur = 0;
+    if ((e = hipGetDevice(&cur)) != hipSuccess) return e;
+    if (cur != dev && (e = hipSetDevice(dev)) != hipSuccess) return e;
+    void* p = nullptr;
+    e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+    const hipError_t e2 = cur != dev ? hipSetDevice(cur) : hipSuccess;
+    if (e != hipSuccess) return e;
+    if (e2 != hipSuccess) return e2;
+    if (!p) return hipErrorInvalidSymbol;
+    g_scratch_ptr[dev] = static_cast<float*>(p);
+  }
+  *ptr = g_scratch_ptr[dev];
+  return hipSuccess;
+}
 
 hipError_t launch_bsattn_bwd(const void* q, const void* k, const void* v, const void* o,
                              const void* dout, const float* lse, void* dq, void* dk, void* dv,

@@ -57,6 +57,14 @@ hipError_t launch_bsattn_bwd(const void* q, const void* k, const void* v, const 
                              const int32_t* colptr, const int32_t* rows, float* delta,
                              hipStream_t s);
 
+// Scratch of ut_bsattn_bwd_noalloc: a file-scope device array in
+// bsattn_bwd.hip, one copy per GPU, holding the backward's two statistics
+// planes (8 bytes per query row).
+constexpr size_t kNoallocScratchBytes = (size_t)32 << 20;
+// Device address of that array on the device that `s` belongs to (the current
+// device for the null stream), looked up once per device.
+hipError_t noalloc_scratch(hipStream_t s, float** ptr);
+
 // ---- Top-K block selection (topk_mask.hip) ----
 constexpr int64_t kTopkMaxLds = 65536;   // LDS bytes of one selection workgroup
 // Query blocks per selection workgroup (16, 4 or 1), 0 if one row does not fit.

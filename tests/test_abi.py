@@ -93,6 +93,22 @@ def test_bwd_rejects_non_positive_scale():
         assert "softmax_scale" in ut.last_error()
 
 
+def test_bwd_noalloc_rejects_problems_beyond_its_scratch():
+    lib = ut.lib()
+    args = [FAKE] * 9
+    tail = [FAKE] * 4 + [0.0883883476]
+    # 1 x 24 x 174763 = 4,194,312 query rows > 4,194,304 (32 MiB of 8-byte rows)
+    st = lib.ut_bsattn_bwd_noalloc(*args, 1, 174763, 24, 128, 128, *tail, None)
+    assert st == ut.UT_ERR_WORKSPACE and "built-in scratch" in ut.last_error()
+    st = lib.ut_bsattn_bwd_noalloc(*args, 2, 100000, 24, 128, 128, *tail, None)
+    assert st == ut.UT_ERR_WORKSPACE
+    # the usual checks come first
+    assert lib.ut_bsattn_bwd_noalloc(*args, 1, 100, 2, 96, 128, *tail, None) == ut.UT_ERR_UNSUPPORTED
+    args[6] = None
+    assert lib.ut_bsattn_bwd_noalloc(*args, 1, 100, 2, 128, 128, *tail, None) == ut.UT_ERR_INVALID_ARG
+    assert "dq is NULL" in ut.last_error()
+
+
 def _fwd_varlen(**kw):
     a = dict(q=FAKE, k=FAKE, v=FAKE, o=FAKE, lse=FAKE, cu=FAKE, B=3, T=300, maxlen=128, H=2, D=128,
              block=128, rowptr=FAKE, cols=FAKE, scale=0.1)
