@@ -22,6 +22,14 @@ __device__ inline f32x16 mfma32(bf16x8 a, bf16x8 b, f32x16 c) {
   return __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, b, c, 0, 0, 0);
 }
 
+// D = A(16x32) * B(32x16) + C. Lane l holds A[l%16][8(l/16)+e],
+// B[8(l/16)+e][l%16] (e = 0..7) and C[4(l/16) + i][l%16] (i = 0..3).
+// At equal FLOPs this shape draws less power than the 32x32x16 one: under the
+// board's power limit it sustains a higher clock on random operands.
+__device__ inline f32x4 mfma16(bf16x8 a, bf16x8 b, f32x4 c) {
+  return __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, b, c, 0, 0, 0);
+}
+
 // Transposing LDS read: in each 16-lane group, lanes 4r..4r+3 address row r
 // (four consecutive 16-bit elements each); lane j receives element j of the
 // 16-element rows r = 0..3.
@@ -39,6 +47,25 @@ __device__ inline float pair_sum(float x) {
   return __uint_as_float(r[0]) + __uint_as_float(r[1]);
 }
 
+// Combined over the four 16-lane groups (lanes l, l^16, l^32, l^48).
+__device__ inline float quad_max(float x) {
+  x = pair_max(x);
+  const auto r = __builtin_amdgcn_permlane16_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+  return fmaxf(__uint_as_float(r[0]), __uint_as_float(r[1]));
+}
+__device__ inline float quad_sum(float x) {
+  x = pair_sum(x);
+  const auto r = __builtin_amdgcn_permlane16_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+  return __uint_as_float(r[0]) + __uint_as_float(r[1]);
+}
+
+// Two floats rounded to bf16 (nearest even) and packed, a in the low half.
+__device__ inline unsigned pack_bf16x2(float a, float b) {
+  typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
+  const bf16x2 v = {(__bf16)a, (__bf16)b};
+  return __builtin_bit_cast(unsigned, v);
+}
+
 __device__ inline float fast_exp2(float x) { return __builtin_amdgcn_exp2f(x); }
 
 // LDS byte offset of logical 16-byte chunk c of row r in a tile of CPR chunks
@@ -50,6 +77,21 @@ template <int CPR>
 __device__ inline int lds_off(int r, int c) {
   static_assert(CPR == 16 || CPR == 8, "rows of 128 or 64 bf16");
   const int sw = CPR == 16 ? (((r & 3) << 2) | ((r >> 2) & 3)) : ((r >> 1) & 7);
+  return r * CPR * 16 + ((c ^ sw) << 4);
+}
+
+// LDS byte offset of logical 16-byte chunk c of row r for the 16x16x32
+// kernels. Their two access patterns are b128 reads of one chunk over 16
+// consecutive rows (one per 16-lane group) and transposing 8-byte reads of
+// rows 4g..4g+3 (lane group g) over two adjacent chunks, where a half-wave
+// covers 8 rows. The swizzle is a permutation over any 16 consecutive rows
+// (first pattern) whose value >> 1 differs between the 8 rows of either half
+// (second pattern), so neither pattern has bank conflicts.
+template <int CPR>
+__device__ inline int swz_off(int r, int c) {
+  static_assert(CPR == 16 || CPR == 8, "rows of 128 or 64 bf16");
+  const int sw = CPR == 16 ? (((r & 7) << 1) | ((r >> 3) & 1))
+                           : ((((r >> 1) & 3) << 1) | ((r >> 3) & 1));
   return r * CPR * 16 + ((c ^ sw) << 4);
 }
 

@@ -7,9 +7,16 @@
 // two workgroups share a CU, so each SIMD runs two independent waves.
 // Scores are formed transposed, S^T = K Q^T, with 32x32x16 bf16 MFMA: each
 // lane holds one query column (16 keys per 32x32 tile), so row max and row
-// sum are in-lane plus one permlane32 swap, and the probabilities feed the
-// second product O^T += V^T P^T straight from registers as the B operand.
-// V^T operands come from LDS with the transposing ds_read_b64_tr_b16.
+// sum are in-lane plus one permlane32 swap. The second product
+// O^T += V^T P^T runs on 16x16x32 bf16 MFMA, the shape that draws less power
+// per FLOP (under the board's power limit it holds a higher clock): one
+// v_permlane16_swap per register moves the probabilities from the score
+// layout (lane = one query, 16 keys) to the B-operand layout of two 16-query
+// groups (lane = one query of each group, 8 keys), with the keys in an
+// order whose V^T operand the transposing ds_read_b64_tr_b16 reads without
+// bank conflicts. (The score product stays on 32x32x16: its K operand read
+// in the 16x16x32 layout, four lane groups on the same 16 rows, costs LDS
+// bank-conflict cycles.)
 //
 // The loop is built to spend as few vector instructions per MFMA as
 // possible, since the vector ALU (softmax) and not the matrix core is the
@@ -51,7 +58,7 @@ struct FwdCfg {
   static constexpr int RPI = 1024 / ROWB;        // rows per direct-load instruction
   static constexpr int IPW = TILEB / 1024 / NW;  // direct-load instructions per wave per tile
   static constexpr int KS = D / 16;              // k-steps of the score product
-  static constexpr int DT = D / 32;              // 32-wide d tiles of O
+  static constexpr int DT = D / 16;              // 16-wide d tiles of O
   static_assert(TILEB % (1024 * NW) == 0, "tile must split evenly over the waves");
 };
 
@@ -92,12 +99,10 @@ __global__ __launch_bounds__(64 * (BLOCK / 32), (BLOCK == 128 || D == 64) ? 2 : 
 
   if (T == 0) {  // empty S_i: O = 0, LSE = -inf
     if (q < N) {
-      const bf16x4 z = {};
+      const bf16x8 z = {};
 #pragma unroll
-      for (int dt = 0; dt < C::DT; ++dt)
-#pragma unroll
-        for (int a = 0; a < 4; ++a)
-          *reinterpret_cast<bf16x4*>(O + base_bh + q * tok_stride + 32 * dt + 8 * a + 4 * g) = z;
+      for (int dc = 0; dc < D / 16; ++dc)   // this lane: 8 columns of 16 per half
+        *reinterpret_cast<bf16x8*>(O + base_bh + q * tok_stride + 16 * dc + 8 * g) = z;
       if (g == 0) LSE[sr.stat0 + q] = -INFINITY;
     }
     return;
@@ -141,22 +146,26 @@ __global__ __launch_bounds__(64 * (BLOCK / 32), (BLOCK == 128 || D == 64) ? 2 : 
   int koff[C::KS];
 #pragma unroll
   for (int ks = 0; ks < C::KS; ++ks) koff[ks] = lds_off<C::CPR>(l32, 2 * ks + g);
-  const int jr = lane & 15;
-  const int dsub = 16 * ((lane >> 4) & 1) + 4 * (jr & 3);
-  int voff[C::DT][2];
+  // V^T operand of the 16x16x32 product for d tile dt, key step kc (32
+  // keys): lane group gq = lane / 16 reads rows 32 kc + base(gq) + (c16 >> 2)
+  // (slots 0..3) and the same + 16 (slots 4..7), columns 16 dt + 4 (c16 & 3)
+  // .. +3, base(gq) = 8 (gq & 1) + 4 (gq >> 1): the keys the P exchange
+  // below leaves in that lane group. Rows 16 apart share the swizzle, so kc and
+  // the +16 are immediates.
+  const int c16 = lane & 15, gq = lane >> 4;
+  int voff[C::DT];
 #pragma unroll
-  for (int dt = 0; dt < C::DT; ++dt)
-#pragma unroll
-    for (int lh = 0; lh < 2; ++lh) {
-      const int r0 = 4 * g + (jr >> 2) + 8 * lh;
-      const int d = 32 * dt + dsub;
-      voff[dt][lh] = lds_off<C::CPR>(r0, d >> 3) + 2 * (d & 7);
-    }
+  for (int dt = 0; dt < C::DT; ++dt) {
+    const int d = 16 * dt + 4 * (c16 & 3);
+    voff[dt] = lds_off<C::CPR>(8 * (gq & 1) + 4 * (gq >> 1) + (c16 >> 2), d >> 3) + 2 * (d & 7);
+  }
 
   const float c2 = scale * kLog2e;   // scores in log2 units
-  f32x16 oacc[C::DT];
+  // O^T in the 16x16 layout: oacc[dt][qg] lane holds
+  // O^T[16 dt + 4 gq + (0..3)][query 32 w + 16 qg + c16]
+  f32x4 oacc[C::DT][2];
 #pragma unroll
-  for (int dt = 0; dt < C::DT; ++dt) oacc[dt] = f32x16{};
+  for (int dt = 0; dt < C::DT; ++dt) oacc[dt][0] = oacc[dt][1] = f32x4{};
   float m_run = -INFINITY, l_run = 0.f;
 
   // One sub-tile: S^T = K Q^T, online softmax, O^T += V^T P^T. Rows 32 kt + l32
@@ -183,7 +192,10 @@ __global__ __launch_bounds__(64 * (BLOCK / 32), (BLOCK == 128 || D == 64) ? 2 : 
     }
     // Exponentials against the running max; the max itself is taken only on
     // the first tile or when a tile's sum leaves the guard (rare).
-    bf16x8 pb[2][2];
+    // pq[kt][0]: elements 0-3, 8-11 (keys 32 kt + 4 g + {0..3, 16..19}),
+    // pq[kt][1]: elements 4-7, 12-15 (keys 32 kt + 4 g + {8..11, 24..27}),
+    // as bf16 pairs (elements e, e + 1 in one register)
+    u32x4 pq[2][2];
     float lsum = 0.f;
     auto expo = [&]() __attribute__((always_inline)) {
       const float m_use = m_run == -INFINITY ? 0.f : m_run;
@@ -191,12 +203,28 @@ __global__ __launch_bounds__(64 * (BLOCK / 32), (BLOCK == 128 || D == 64) ? 2 : 
 #pragma unroll
       for (int kt = 0; kt < 2; ++kt)
 #pragma unroll
-        for (int e = 0; e < 16; ++e) {
-          const float p = fast_exp2(__builtin_fmaf(s[kt][e], c2, -m_use));
-          lsum += p;
-          pb[kt][e >> 3][e & 7] = (__bf16)p;
+        for (int e = 0; e < 16; e += 2) {
+          const float p0 = fast_exp2(__builtin_fmaf(s[kt][e], c2, -m_use));
+          const float p1 = fast_exp2(__builtin_fmaf(s[kt][e + 1], c2, -m_use));
+          lsum += p0;
+          lsum += p1;
+          pq[kt][(e >> 2) & 1][((e & 3) >> 1) + 2 * (e >> 3)] = pack_bf16x2(p0, p1);
         }
     };
+    // V^T operands of the second product, pair pp = (dt, kc) = (pp / 2,
+    // pp % 2): the first kPre pairs are read here, so that their latency hides
+    // behind the softmax; the rest are read kPre pairs ahead of their use.
+    constexpr int kPairs = 2 * C::DT, kPre = 4;
+    bf16x8 vop[kPre];
+    auto read_v = [&](int pp) __attribute__((always_inline)) {
+      const char* vb = vt_lds + 32 * (pp & 1) * C::ROWB + voff[pp >> 1];
+      const s16x4 lo = lds_read_tr16(vb);
+      const s16x4 hi = lds_read_tr16(vb + 16 * C::ROWB);
+      const s16x8 v8 = {lo[0], lo[1], lo[2], lo[3], hi[0], hi[1], hi[2], hi[3]};
+      return __builtin_bit_cast(bf16x8, v8);
+    };
+#pragma unroll
+    for (int pp = 0; pp < kPre; ++pp) vop[pp] = read_v(pp);
     bool redo = __ballot(m_run == -INFINITY) != 0;
     if (!redo) {
       expo();
@@ -209,29 +237,56 @@ __global__ __launch_bounds__(64 * (BLOCK / 32), (BLOCK == 128 || D == 64) ? 2 : 
 #pragma unroll
         for (int e = (kt == 0 ? 1 : 0); e < 16; ++e) mx = fmaxf(mx, s[kt][e]);
       mx = pair_max(mx) * c2;
+      float alpha = 1.f;
       if (mx > m_run) {
-        const float alpha = fast_exp2(m_run - mx);   // 0 on the first tile
+        alpha = fast_exp2(m_run - mx);   // 0 on the first tile
         l_run *= alpha;
-#pragma unroll
-        for (int dt = 0; dt < C::DT; ++dt) oacc[dt] *= alpha;
         m_run = mx;
+      }
+      // O^T columns are queries c16 (qg 0, held in the even 16-lane row of
+      // each pair in the score layout) and 16 + c16 (qg 1, the odd row)
+      const auto ar = __builtin_amdgcn_permlane16_swap(__float_as_uint(alpha),
+                                                       __float_as_uint(alpha), false, false);
+#pragma unroll
+      for (int dt = 0; dt < C::DT; ++dt) {
+        oacc[dt][0] *= __uint_as_float(ar[0]);
+        oacc[dt][1] *= __uint_as_float(ar[1]);
       }
       expo();
     }
     l_run += lsum;
-    // O^T += V^T P^T: P^T tile kt, half hh covers keys 32kt + 16hh + {4g+0..3, 8+4g+0..3}
+    // P^T to the B-operand layout of two 16-query groups: the swap leaves in
+    // register 0 (qg 0) and 1 (qg 1) of 16-lane row gq the keys
+    // 32 kt + base(gq) + {0..3, 16..19} of queries c16 and 16 + c16.
+    bf16x8 pop[2][2];
 #pragma unroll
-    for (int dt = 0; dt < C::DT; ++dt)
+    for (int kt = 0; kt < 2; ++kt) {
+      const u32x4 a = pq[kt][0], b = pq[kt][1];
+      u32x4 na, nb;
 #pragma unroll
-      for (int kt = 0; kt < 2; ++kt)
+      for (int v = 0; v < 4; ++v) {
+        const auto r = __builtin_amdgcn_permlane16_swap(a[v], b[v], false, false);
+        na[v] = r[0];
+        nb[v] = r[1];
+      }
+      pop[kt][0] = __builtin_bit_cast(bf16x8, na);
+      pop[kt][1] = __builtin_bit_cast(bf16x8, nb);
+    }
+    // O^T += V^T P^T over the two 32-key steps, operands kPre pairs ahead
 #pragma unroll
-        for (int hh = 0; hh < 2; ++hh) {
-          const char* vb = vt_lds + (32 * kt + 16 * hh) * C::ROWB;
-          const s16x4 lo = lds_read_tr16(vb + voff[dt][0]);
-          const s16x4 hi = lds_read_tr16(vb + voff[dt][1]);
-          const s16x8 v8 = {lo[0], lo[1], lo[2], lo[3], hi[0], hi[1], hi[2], hi[3]};
-          oacc[dt] = mfma32(__builtin_bit_cast(bf16x8, v8), pb[kt][hh], oacc[dt]);
-        }
+    for (int pp = 0; pp < kPairs; ++pp) {
+      const bf16x8 av = vop[pp % kPre];
+      if (pp + kPre < kPairs) vop[pp % kPre] = read_v(pp + kPre);
+      oacc[pp >> 1][0] = mfma16(av, pop[pp & 1][0], oacc[pp >> 1][0]);
+      oacc[pp >> 1][1] = mfma16(av, pop[pp & 1][1], oacc[pp >> 1][1]);
+    }
+    // keep that order: two products, then the two reads of a later pair
+#pragma unroll
+    for (int pp = 0; pp + kPre < kPairs; ++pp) {
+      __builtin_amdgcn_sched_group_barrier(0x008, 2, 0);   // MFMA
+      __builtin_amdgcn_sched_group_barrier(0x100, 2, 0);   // DS read
+    }
+    __builtin_amdgcn_sched_group_barrier(0x008, 2 * kPre, 0);
   };
 
   // Iteration t: issue the loads of tile t+1 into the other stage (read in
@@ -286,17 +341,23 @@ __global__ __launch_bounds__(64 * (BLOCK / 32), (BLOCK == 128 || D == 64) ? 2 : 
   // ---- epilogue: O = O^T / l, LSE = (m + log2 l) ln 2
   const float l_tot = pair_sum(l_run);
   const float inv = l_tot > 0.f ? 1.f / l_tot : 0.f;
-  if (q < N) {
+  if (q < N && g == 0) LSE[sr.stat0 + q] = l_tot > 0.f ? (m_run + __log2f(l_tot)) * kLn2 : -INFINITY;
+  // 1/l of queries c16 (qg 0) and 16 + c16 (qg 1) for the 16x16 layout
+  const auto ir = __builtin_amdgcn_permlane16_swap(__float_as_uint(inv), __float_as_uint(inv),
+                                                   false, false);
 #pragma unroll
-    for (int dt = 0; dt < C::DT; ++dt)
+  for (int qg = 0; qg < 2; ++qg) {
+    const int qo = i * BLOCK + 32 * w + 16 * qg + c16;
+    const float iv = __uint_as_float(ir[qg]);
+    if (qo < N) {
 #pragma unroll
-      for (int a = 0; a < 4; ++a) {
+      for (int dt = 0; dt < C::DT; ++dt) {
         bf16x4 v4;
 #pragma unroll
-        for (int e = 0; e < 4; ++e) v4[e] = (__bf16)(oacc[dt][4 * a + e] * inv);
-        *reinterpret_cast<bf16x4*>(O + base_bh + q * tok_stride + 32 * dt + 8 * a + 4 * g) = v4;
+        for (int e = 0; e < 4; ++e) v4[e] = (__bf16)(oacc[dt][qg][e] * iv);
+        *reinterpret_cast<bf16x4*>(O + base_bh + qo * tok_stride + 16 * dt + 4 * gq) = v4;
       }
-    if (g == 0) LSE[sr.stat0 + q] = l_tot > 0.f ? (m_run + __log2f(l_tot)) * kLn2 : -INFINITY;
+    }
   }
 }
 
