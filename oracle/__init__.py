@@ -125,15 +125,17 @@ def block_index(block_mask: np.ndarray):
 # Block-sparse attention (Sec. 3.3, Eq. 5 and Eq. 8)
 # ---------------------------------------------------------------------------
 
-def _f64(x) -> np.ndarray:
-    """Exact upcast of a bf16 torch tensor (or any array) to float64."""
+def _f64(x, dtype=np.float64) -> np.ndarray:
+    """Exact upcast of a bf16 torch tensor (or any array) to float64 (or to
+    float32, also exact for bf16 inputs)."""
     try:
         import torch
         if isinstance(x, torch.Tensor):
-            return x.detach().to(torch.float64).numpy()
+            tt = torch.float64 if np.dtype(dtype) == np.float64 else torch.float32
+            return x.detach().to(tt).numpy()
     except ImportError:  # pragma: no cover
         pass
-    return np.asarray(x, dtype=np.float64)
+    return np.asarray(x, dtype=dtype)
 
 
 def _block_tokens(j: int, block: int, n: int) -> np.ndarray:
@@ -152,7 +154,7 @@ def _selected_keys(mask_row: np.ndarray, block: int, n: int) -> np.ndarray:
 
 
 def bsattn_fwd(q, k, v, block_mask, block: int, scale: float,
-               q_blocks=None):
+               q_blocks=None, dtype=np.float64):
     """Eq. 8: O_i = softmax(Q_i K_{S_i}^T * scale) V_{S_i} per (batch, head,
     query block i), plus the natural-log log-sum-exp of each query row's
     scaled scores over the keys it attends to.
@@ -163,14 +165,16 @@ def bsattn_fwd(q, k, v, block_mask, block: int, scale: float,
     empty attends to nothing: its rows are O = 0 and LSE = -inf (the paper
     never produces such a row; this is the reading taken).
 
-    Returns (O [B, N, H, D], LSE [B, H, N]) in float64.
+    Returns (O [B, N, H, D], LSE [B, H, N]) in float64. dtype=np.float32
+    runs the same arithmetic in float32 (used only to time a CPU baseline;
+    every check uses float64).
     """
-    Q, K, V = _f64(q), _f64(k), _f64(v)
+    Q, K, V = _f64(q, dtype), _f64(k, dtype), _f64(v, dtype)
     m = np.asarray(block_mask)
     B, N, H, D = Q.shape
     Nq = m.shape[2]
-    O = np.full((B, N, H, D), np.nan)
-    LSE = np.full((B, H, N), np.nan)
+    O = np.full((B, N, H, D), np.nan, dtype=dtype)
+    LSE = np.full((B, H, N), np.nan, dtype=dtype)
     blocks = range(Nq) if q_blocks is None else q_blocks
     for b in range(B):
         for h in range(H):
@@ -181,7 +185,7 @@ def bsattn_fwd(q, k, v, block_mask, block: int, scale: float,
                     O[b, rows, h, :] = 0.0
                     LSE[b, h, rows] = -np.inf
                     continue
-                S = (Q[b, rows, h, :] @ K[b, keys, h, :].T) * scale
+                S = (Q[b, rows, h, :] @ K[b, keys, h, :].T) * Q.dtype.type(scale)
                 mx = S.max(axis=1, keepdims=True)
                 E = np.exp(S - mx)
                 l = E.sum(axis=1, keepdims=True)
@@ -191,7 +195,7 @@ def bsattn_fwd(q, k, v, block_mask, block: int, scale: float,
 
 
 def bsattn_bwd(q, k, v, dout, block_mask, block: int, scale: float,
-               q_blocks=None):
+               q_blocks=None, dtype=np.float64):
     """Gradients of Eq. 8 for a loss whose gradient w.r.t. O is dout.
 
     The block mask is a constant. With P = softmax(S) over the retained keys of
@@ -203,15 +207,17 @@ def bsattn_bwd(q, k, v, dout, block_mask, block: int, scale: float,
 
     q_blocks: optional subset of query blocks whose contributions are summed
     (dQ of other rows is NaN; dK and dV then hold only the listed blocks'
-    contributions). Returns (dQ, dK, dV) [B, N, H, D] float64.
+    contributions). Returns (dQ, dK, dV) [B, N, H, D] float64 (float32 with
+    dtype=np.float32, as for bsattn_fwd).
     """
-    Q, K, V, dO = _f64(q), _f64(k), _f64(v), _f64(dout)
+    Q, K, V, dO = _f64(q, dtype), _f64(k, dtype), _f64(v, dtype), _f64(dout, dtype)
     m = np.asarray(block_mask)
     B, N, H, D = Q.shape
     Nq = m.shape[2]
-    dQ = np.full((B, N, H, D), np.nan)
-    dK = np.zeros((B, N, H, D))
-    dV = np.zeros((B, N, H, D))
+    sc = Q.dtype.type(scale)
+    dQ = np.full((B, N, H, D), np.nan, dtype=dtype)
+    dK = np.zeros((B, N, H, D), dtype=dtype)
+    dV = np.zeros((B, N, H, D), dtype=dtype)
     blocks = range(Nq) if q_blocks is None else q_blocks
     for b in range(B):
         for h in range(H):
@@ -222,14 +228,14 @@ def bsattn_bwd(q, k, v, dout, block_mask, block: int, scale: float,
                 if keys.size == 0:
                     continue
                 Qi, Kk, Vk, dOi = Q[b, rows, h], K[b, keys, h], V[b, keys, h], dO[b, rows, h]
-                S = (Qi @ Kk.T) * scale
+                S = (Qi @ Kk.T) * sc
                 E = np.exp(S - S.max(axis=1, keepdims=True))
                 P = E / E.sum(axis=1, keepdims=True)
                 dP = dOi @ Vk.T
                 delta = (P * dP).sum(axis=1, keepdims=True)
                 dS = P * (dP - delta)
-                dQ[b, rows, h, :] = scale * (dS @ Kk)
-                dK[b, keys, h, :] += scale * (dS.T @ Qi)
+                dQ[b, rows, h, :] = sc * (dS @ Kk)
+                dK[b, keys, h, :] += sc * (dS.T @ Qi)
                 dV[b, keys, h, :] += P.T @ dOi
     return dQ, dK, dV
 

@@ -315,6 +315,32 @@ def test_bwd_matches_torch_autograd(seed, n, block, H, D, density):
     assert np.allclose(dV, tv.grad.numpy(), atol=1e-12)
 
 
+def test_fp32_arithmetic_option_matches_fp32_sdpa_and_autograd():
+    """The float32 option (CPU-baseline timing only) against torch's float32
+    SDPA and autograd on bf16-exact inputs: same definition, fp32 rounding."""
+    rng = np.random.default_rng(9)
+    n, block, H, D = 150, 32, 2, 16
+    q, k, v, do = (torch.tensor(rng.standard_normal((1, n, H, D)), dtype=torch.float32)
+                   .to(torch.bfloat16) for _ in range(4))
+    nb = -(-n // block)
+    bm = (rng.random((1, H, nb, nb)) < 0.4).astype(np.uint8)
+    bm[:, :, np.arange(nb), np.arange(nb)] = 1
+    tq, tk, tv = (x.float().clone().requires_grad_(True) for x in (q, k, v))
+    t = lambda a: a.permute(0, 2, 1, 3)
+    o = torch.nn.functional.scaled_dot_product_attention(
+        t(tq), t(tk), t(tv), attn_mask=torch.as_tensor(_expand_mask(bm, n, block)))
+    o.permute(0, 2, 1, 3).backward(do.float())
+    sc = 1.0 / math.sqrt(D)
+    O, LSE = oracle.bsattn_fwd(q, k, v, bm, block, sc, dtype=np.float32)
+    dQ, dK, dV = oracle.bsattn_bwd(q, k, v, do, bm, block, sc, dtype=np.float32)
+    assert O.dtype == np.float32 and dQ.dtype == np.float32
+    assert np.allclose(O, o.permute(0, 2, 1, 3).detach().numpy(), atol=2e-6, rtol=1e-5)
+    for got, ref in ((dQ, tq.grad), (dK, tk.grad), (dV, tv.grad)):
+        assert np.allclose(got, ref.numpy(), atol=2e-5, rtol=1e-4)
+    O64, LSE64 = oracle.bsattn_fwd(q, k, v, bm, block, sc)
+    assert np.abs(LSE - LSE64).max() < 1e-5
+
+
 def test_bwd_central_finite_differences():
     rng = np.random.default_rng(21)
     n, block, H, D = 19, 6, 1, 3
