@@ -12,8 +12,15 @@ Inputs are resident in HBM before the timed region.
 
 `value` is effective TFLOP/s: the algorithmic FLOPs of attention forward +
 backward over retained block pairs only (forward 4 r c d per pair, backward
-2.5x that) divided by the time of the whole step. The roofline object is the
-forward kernel's, timed with HIP events on the stream it runs on.
+2.5x that) divided by the time of the whole step. The library's tracing aid
+times every kernel launch of the timed steps with HIP events on the stream it
+runs on; `roofline` is the step's dominant kernel and `kernels` lists each
+attention and copy kernel against its own roofline. `sweep` times the other
+workload configurations, `cpu_baseline` the float32 oracle on this host.
+
+Other modes: --ceiling runs the MFMA-rate probe (the sustained matrix-core
+rate under the board's power limit) and --power samples board power and
+clocks with amd-smi while each attention call loops.
 """
 from __future__ import annotations
 
@@ -31,30 +38,38 @@ PEAK_BF16_TFLOPS = 2516.6     # MI355X dense bf16 MFMA (256 CU x 2.4 GHz x 4096 
 PEAK_HBM_GBS = 8000.0
 CAL_COPY_BYTES = 1 << 28      # calibration copy: 256 MiB read + 256 MiB written
 
-# HBM-side bytes of one forward launch on c2k_train at rho = 0.1, from
-# rocprofv3 FETCH_SIZE and WRITE_SIZE passes over this script (per dispatch,
-# scaled by what the counters read for the calibration copy: x2.0 and x1.0).
-# They describe the kernel built from the sources hashed here; any change to
-# those sources makes the figure stale and `traffic` is then reported as null.
-FWD_TRAFFIC = {
+# Counter-measured figures of each kernel on the 2K training workload at
+# rho = 0.1 (profiles/bsattn_c2k_train_rho0.1_*): HBM-side bytes per dispatch
+# from rocprofv3 FETCH_SIZE and WRITE_SIZE passes over this script (scaled by
+# what the counters read for the calibration copy, x2.0 and x1.0) and the
+# sustained clock (GRBM_GUI_ACTIVE per XCD over the dispatch time). Each entry
+# describes the kernel built from the sources whose SHA-256 is listed with it;
+# once those sources change, its figures are reported as null.
+PROFILED = {
     "workload": "c2k_train", "rho": "0.1",
-    "read_bytes": 43.681e9, "write_bytes": 0.487e9,
-    "sources": ("bsattn_fwd.hip", "attn_util.h"),
-    "sha256": "28c95bcf8fadd0947a6220c824582081dd1d3be5630ae94c23cd8eada1808b33",
+    "sources": {},
+    "kernels": {},
 }
 
 
-def fwd_traffic(workload: str, rho: str):
-    """Counter-measured HBM bytes per forward launch, or None if stale."""
+def _sources_sha(files) -> str:
     import hashlib
-    t = FWD_TRAFFIC
-    if workload.split("@")[0] != t["workload"] or str(rho) != t["rho"]:
-        return None
     h = hashlib.sha256()
-    for f in t["sources"]:
+    for f in files:
         with open(os.path.join(ROOT, "paper_2609_23169_amd", "csrc", f), "rb") as fh:
             h.update(fh.read())
-    return t["read_bytes"] + t["write_bytes"] if h.hexdigest() == t["sha256"] else None
+    return h.hexdigest()
+
+
+def profiled(kernel: str, workload: str, rho: str) -> dict:
+    """{read_bytes, write_bytes, clock_ghz} of `kernel` if the committed
+    counter figures describe the kernel as built now and this workload."""
+    t = PROFILED
+    k = t["kernels"].get(kernel)
+    if not k or workload != t["workload"] or str(rho) != t["rho"]:
+        return {}
+    files, sha = t["sources"][k["sources"]]
+    return k if _sources_sha(files) == sha else {}
 
 
 def parse():
@@ -65,17 +80,48 @@ def parse():
     ap.add_argument("--workload", default="c2k_train")
     ap.add_argument("--rho", default="0.1")
     ap.add_argument("--no-cpu-baseline", action="store_true")
-    # the packed-sample timing launches the step's attention kernels again at
-    # other shapes; leave it out when a kernel trace should hold the step's only
+    # the packed-sample timing and the sweep launch the step's attention
+    # kernels again at other shapes; leave them out when a kernel trace should
+    # hold the step's only
     ap.add_argument("--no-varlen", action="store_true")
-    ap.add_argument("--cpu-seconds", type=float, default=12.0,
+    ap.add_argument("--no-sweep", action="store_true")
+    ap.add_argument("--sweep-steps", type=int, default=3)
+    ap.add_argument("--cpu-seconds", type=float, default=15.0,
                     help="CPU time budget of the oracle baseline sample")
+    ap.add_argument("--ceiling", action="store_true",
+                    help="only run the MFMA-rate probe and print its JSON line")
+    ap.add_argument("--power", action="store_true",
+                    help="only sample board power and clocks while each attention call loops")
     return ap.parse_args()
 
 
-def cpu_baseline(inst, budget_s: float) -> dict:
-    """The float64 oracle timed on this host on a bounded sample: all query
-    blocks of head 0 in order, forward + backward, until the budget is used."""
+def _host_cpu() -> dict:
+    model = ""
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    model = line.split(":", 1)[1].strip()
+                    break
+    except OSError:
+        pass
+    try:
+        logical = len(os.sched_getaffinity(0))
+    except Exception:
+        logical = os.cpu_count() or 1
+    try:
+        import psutil
+        physical = psutil.cpu_count(logical=False)
+    except Exception:
+        physical = None
+    return {"cpu_model": model, "logical_cpus_available": logical,
+            "physical_cores_host": physical}
+
+
+def cpu_baseline(inst, budget_s: float, step_flops: float) -> dict:
+    """The oracle in float32 timed on this host on a bounded sample: the query
+    blocks of head 0 in order, forward + backward, until the budget is used;
+    the full step's attention time is extrapolated from the sample's rate."""
     import numpy as np
     import oracle
     import workloads as W
@@ -86,25 +132,30 @@ def cpu_baseline(inst, budget_s: float) -> dict:
     bm = inst.block_mask[:, :1]
     nb = bm.shape[-1]
     sizes = W.block_sizes(n, blk)
+    sc = 1 / math.sqrt(wl.head_dim)
     done, flops, t0 = 0, 0, time.perf_counter()
     while done < nb and time.perf_counter() - t0 < budget_s:
         chunk = list(range(done, min(nb, done + 8)))
-        oracle.bsattn_fwd(q, k, v, bm, blk, 1 / math.sqrt(wl.head_dim), q_blocks=chunk)
-        oracle.bsattn_bwd(q, k, v, do, bm, blk, 1 / math.sqrt(wl.head_dim), q_blocks=chunk)
+        oracle.bsattn_fwd(q, k, v, bm, blk, sc, q_blocks=chunk, dtype=np.float32)
+        oracle.bsattn_bwd(q, k, v, do, bm, blk, sc, q_blocks=chunk, dtype=np.float32)
         pairs = int(np.einsum("ij,i,j->", bm[0, 0, chunk].astype(np.int64), sizes[chunk], sizes))
         flops += int(3.5 * 4 * wl.head_dim * pairs)
         done = chunk[-1] + 1
     dt = time.perf_counter() - t0
     try:
         import threadpoolctl
-        cores = max(i.get("num_threads", 1) for i in threadpoolctl.threadpool_info()) or 1
+        threads = max(i.get("num_threads", 1) for i in threadpoolctl.threadpool_info()) or 1
     except Exception:
-        cores = os.cpu_count() or 1
-    return {"value": round(flops / dt / 1e12, 6), "unit": "TFLOP/s", "cores": int(cores),
-            "kind": "oracle",
-            "sample": f"float64 oracle forward+backward, head 0 of 24, query blocks 0..{done - 1} "
-                      f"of {nb} ({done / nb / 24:.2%} of the step's attention work), "
-                      f"{dt:.1f} s wall"}
+        threads = os.cpu_count() or 1
+    rate = flops / dt
+    out = {"value": round(rate / 1e12, 6), "unit": "TFLOP/s", "cores": int(threads),
+           "kind": "oracle",
+           "sample": f"float32 oracle forward+backward, head 0 of {wl.heads}, query blocks "
+                     f"0..{done - 1} of {nb} ({flops / step_flops:.2%} of the step's attention "
+                     f"work), {dt:.1f} s wall; cores = BLAS threads used"}
+    out.update(_host_cpu())
+    out["extrapolated_step_attention_s"] = round(step_flops / rate, 1)
+    return out
 
 
 def time_topk(ut, q, k, blk: int, k_keep: int, stream, reps: int = 10) -> dict:
@@ -293,6 +344,214 @@ def time_varlen(ut, W, dev, stream, count: int = 8, reps: int = 10) -> dict:
             "tflops_one_by_one": round(tot / (ms_loop * 1e-3) / 1e12, 2)}
 
 
+def kernel_rooflines(trace: list, steps: int, F: float, n: int, H: int, D: int,
+                     row_bytes: int, workload: str, rho: str) -> list:
+    """Each attention and copy kernel of the timed steps against its own
+    roofline. Algorithmic work per launch (F = forward FLOPs, 4 r c d per
+    retained pair): forward F; dK/dV its S, dP, dV and dK products, 2 F; dQ
+    its dQ product, F / 2 (it also recomputes S and dP, which are not
+    counted); the pre-pass reads O, dO and LSE and writes two fp32 planes;
+    gather and scatter read and write every kept row once."""
+    out = []
+    for r in trace:
+        nm = r["name"]
+        if nm.startswith("bsattn_fwd"):
+            bound, work = "mfma", F
+        elif nm.startswith("bwd_dkdv"):
+            bound, work = "mfma", 2 * F
+        elif nm.startswith("bwd_dq"):
+            bound, work = "mfma", F / 2
+        elif nm.startswith("bwd_prep"):
+            bound, work = "hbm", n * H * (2 * D * 2 + 4 + 8)
+        elif nm in ("gather_rows", "scatter_rows"):
+            bound, work = "hbm", 2 * n * row_bytes + 4 * n
+        else:
+            continue
+        ms = r["total_ms"] / r["count"]
+        rate = work / (ms * 1e-3) / (1e12 if bound == "mfma" else 1e9)
+        peak = PEAK_BF16_TFLOPS if bound == "mfma" else PEAK_HBM_GBS
+        prof = profiled(nm, workload, rho)
+        out.append({"kernel": nm, "bound": bound, "ms": round(ms, 4),
+                    "launches_per_step": round(r["count"] / steps, 3),
+                    "share_of_step_kernels": None, "work_per_launch": work,
+                    "achieved": round(rate, 2), "peak": peak,
+                    "unit": "TFLOP/s" if bound == "mfma" else "GB/s",
+                    "frac": round(rate / peak, 4),
+                    "traffic": (prof["read_bytes"] + prof["write_bytes"]) if prof else None,
+                    "clock_ghz": prof.get("clock_ghz") if prof else None,
+                    "total_ms": r["total_ms"]})
+    return out
+
+
+# the other workload configurations, timed after the step: (workload, rho,
+# the passes the configuration is defined with)
+SWEEP = [("c512", "0.3", "fwd"), ("c1k", "0.2", "fwd+bwd"), ("c2k", "0.1", "fwd"),
+         ("c2k_train", "0.05", "fwd+bwd"), ("c2k_train", "0.2", "fwd+bwd"),
+         ("c2k_train", "1", "fwd+bwd")]
+
+
+def sweep(ut, W, dev, stream, base: dict, steps: int) -> list:
+    """Forward and backward times of every other configuration (the backward
+    of forward-only configurations is timed too, for reference). The training
+    workload's rho variants reuse the step's Q, K, V and dO (the same draws)."""
+    import torch
+    out = []
+    for name, rho, passes in SWEEP:
+        wl = W.WORKLOADS[name].with_rho(rho)
+        if name == base["workload"]:
+            inst = W.make(wl, with_qkv=False)
+            q, k, v, do = base["q"], base["k"], base["v"], base["do"]
+        else:
+            inst = W.make(wl, with_do=True)
+            q, k, v, do = (t.to(dev) for t in (inst.q, inst.k, inst.v, inst.do))
+        n, H, D, blk = inst.n_kept, wl.heads, wl.head_dim, wl.block
+        sc = 1.0 / math.sqrt(D)
+        with torch.cuda.stream(stream):
+            idx = ut.build_block_index(torch.from_numpy(inst.block_mask).to(dev))
+            o = torch.empty_like(q)
+            lse = torch.empty((1, H, n), dtype=torch.float32, device=dev)
+            dq, dk, dv = torch.empty_like(q), torch.empty_like(q), torch.empty_like(q)
+            ws = torch.empty(ut.ut_bsattn_bwd_workspace_size(1, n, H), dtype=torch.uint8, device=dev)
+
+            def fwd():
+                st = ut.ut_bsattn_fwd(q, k, v, o, lse, blk, idx["q_rowptr"], idx["q_cols"], sc)
+                if st != ut.UT_OK:
+                    raise ut.UltraTexError("ut_bsattn_fwd", st, ut.last_error())
+
+            def bwd():
+                st = ut.ut_bsattn_bwd(q, k, v, o, do, lse, dq, dk, dv, blk, idx["q_rowptr"],
+                                      idx["q_cols"], idx["kv_colptr"], idx["kv_rows"], sc, ws)
+                if st != ut.UT_OK:
+                    raise ut.UltraTexError("ut_bsattn_bwd", st, ut.last_error())
+
+            fwd(); bwd()
+            torch.cuda.synchronize()
+            ms_f = _time(fwd, stream, steps)
+            ms_b = _time(bwd, stream, steps)
+        F = W.retained_flops_fwd(inst.block_mask, n, blk, D)
+        tf = lambda fl, ms: round(fl / (ms * 1e-3) / 1e12, 2)
+        out.append({"workload": name, "rho": rho, "passes": passes, "tokens": wl.seq_len,
+                    "kept": n, "pairs": int(inst.block_mask.sum()), "fwd_flops": F,
+                    "ms_fwd": round(ms_f, 4), "tflops_fwd": tf(F, ms_f),
+                    "pct_peak_fwd": round(100 * F / (ms_f * 1e-3) / 1e12 / PEAK_BF16_TFLOPS, 2),
+                    "ms_bwd": round(ms_b, 4), "tflops_bwd": tf(2.5 * F, ms_b),
+                    "ms_fwd_bwd": round(ms_f + ms_b, 4), "tflops_fwd_bwd": tf(3.5 * F, ms_f + ms_b),
+                    "pct_peak_fwd_bwd": round(100 * 3.5 * F / ((ms_f + ms_b) * 1e-3) / 1e12
+                                              / PEAK_BF16_TFLOPS, 2),
+                    "steps": steps})
+        del inst, idx, o, lse, dq, dk, dv, ws
+    return out
+
+
+def mfma_ceiling(dev, stream, seconds: float = 2.0) -> dict:
+    """The matrix-core rate the board sustains under its power limit
+    (libutdiag.so): random bf16 operands (shapes 32x32x16 and 16x16x32) and
+    constant ones (32x32x16), each looped for `seconds` before a timed
+    stretch, with the first wave's clock read from s_memtime."""
+    import ctypes
+
+    import torch
+    lib = ctypes.CDLL(os.path.join(ROOT, "paper_2609_23169_amd", "libutdiag.so"))
+    f = lib.ut_diag_mfma_rate
+    f.restype = ctypes.c_int
+    f.argtypes = [ctypes.c_int, ctypes.c_int, ctypes.c_int, ctypes.c_void_p, ctypes.c_void_p,
+                  ctypes.c_void_p, ctypes.c_void_p]
+    cus = torch.cuda.get_device_properties(dev).multi_processor_count
+    grid, iters = 2 * cus, 2000
+    g = torch.Generator(device=dev).manual_seed(11)
+    rnd = torch.randn((grid * 256 * 128,), generator=g, device=dev).to(torch.bfloat16)
+    one = torch.ones_like(rnd)
+    out = torch.empty(grid * 256, dtype=torch.float32, device=dev)
+    clk = torch.zeros(2, dtype=torch.int64, device=dev)
+    flop = grid * 4 * iters * 64 * 32768.0
+    res = {"grid": grid, "waves_per_simd": 2, "flop_per_launch": flop}
+    for key, shape, src in (("bf16_32x32x16_random", 0, rnd), ("bf16_16x16x32_random", 1, rnd),
+                            ("bf16_32x32x16_constant", 0, one)):
+        run = lambda: f(shape, iters, grid, src.data_ptr(), out.data_ptr(), clk.data_ptr(),
+                        ctypes.c_void_p(stream.cuda_stream))
+        if run() != 0:
+            raise RuntimeError(f"ut_diag_mfma_rate({shape}) failed")
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        while time.perf_counter() - t0 < seconds:   # settle the clock under load
+            for _ in range(10):
+                run()
+            torch.cuda.synchronize()
+        ms = _time(run, stream, 20)
+        c = clk.cpu().tolist()
+        res[key] = {"tflops": round(flop / (ms * 1e-3) / 1e12, 1),
+                    "frac_of_peak": round(flop / (ms * 1e-3) / 1e12 / PEAK_BF16_TFLOPS, 4),
+                    "clock_ghz": round(c[0] / c[1] * 0.1, 3) if c[1] else None,
+                    "ms_per_launch": round(ms, 3)}
+    return res
+
+
+def power_sample(ut, dev, stream, q, k, v, do, idx, blk, sc, seconds: float = 6.0) -> dict:
+    """Board power and GFX clocks (amd-smi metric -p -c, sampled about every
+    0.25 s) while each attention call, a 1 GiB device copy and nothing at all
+    loop for `seconds` each."""
+    import re
+    import subprocess
+    import threading
+
+    import torch
+    samples, stop = [], threading.Event()
+
+    def sampler():
+        while not stop.is_set():
+            t = time.time()
+            r = subprocess.run(["amd-smi", "metric", "-p", "-c", "-g", "0"], capture_output=True,
+                               text=True)
+            pw = re.search(r"SOCKET_POWER:\s*([\d.]+)\s*W", r.stdout)
+            clks = [float(x) for x in re.findall(r"GFX_\d+:\s*\n\s*CLK:\s*([\d.]+)\s*MHz", r.stdout)]
+            if pw:
+                samples.append((t, float(pw.group(1)), sum(clks) / len(clks) if clks else None))
+            stop.wait(0.25)
+
+    n, H, D = q.shape[1], q.shape[2], q.shape[3]
+    o = torch.empty_like(q)
+    lse = torch.empty((1, H, n), dtype=torch.float32, device=dev)
+    dq, dk, dv = torch.empty_like(q), torch.empty_like(q), torch.empty_like(q)
+    ws = torch.empty(ut.ut_bsattn_bwd_workspace_size(1, n, H), dtype=torch.uint8, device=dev)
+    big = torch.empty(1 << 30, dtype=torch.uint8, device=dev)
+    big2 = torch.empty_like(big)
+    fwd = lambda: ut.ut_bsattn_fwd(q, k, v, o, lse, blk, idx["q_rowptr"], idx["q_cols"], sc)
+    bwd = lambda: ut.ut_bsattn_bwd(q, k, v, o, do, lse, dq, dk, dv, blk, idx["q_rowptr"],
+                                   idx["q_cols"], idx["kv_colptr"], idx["kv_rows"], sc, ws)
+    phases = [("idle", None), ("forward", fwd), ("backward", bwd), ("copy_1GiB", lambda: big2.copy_(big))]
+    th = threading.Thread(target=sampler, daemon=True)
+    th.start()
+    spans = []
+    for name, fn in phases:
+        t0 = time.time()
+        calls = 0
+        while time.time() - t0 < seconds:
+            if fn is None:
+                time.sleep(0.1)
+                continue
+            for _ in range(5):
+                fn()
+            calls += 5
+            torch.cuda.synchronize()
+        spans.append((name, t0, time.time(), calls))
+        time.sleep(1.0)
+    stop.set()
+    th.join()
+    out = {"sampler": "amd-smi metric -p -c -g 0, about every 0.25 s", "seconds_per_phase": seconds}
+    for name, t0, t1, calls in spans:
+        # the first second of a phase is the clock settling; use the rest
+        sel = [s for s in samples if t0 + 1.0 <= s[0] <= t1]
+        if not sel:
+            continue
+        pw = [s[1] for s in sel]
+        ck = [s[2] for s in sel if s[2] is not None]
+        out[name] = {"samples": len(sel), "socket_power_w_mean": round(sum(pw) / len(pw), 1),
+                     "socket_power_w_max": max(pw),
+                     "gfx_clock_mhz_mean": round(sum(ck) / len(ck), 1) if ck else None,
+                     "calls": calls}
+    return out
+
+
 def main():
     args = parse()
     if args.gpus != 1:
@@ -305,21 +564,31 @@ def main():
     import paper_2609_23169_amd as ut
     import workloads as W
 
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+    if args.ceiling:
+        print(json.dumps({"mfma_ceiling": mfma_ceiling(dev, torch.cuda.current_stream())}), flush=True)
+        return
+
     wl = W.WORKLOADS[args.workload]
     if args.rho:
         wl = wl.with_rho(args.rho)
-    inst = W.make(wl, with_do=True, with_hidden=bool(wl.hidden))
-    dev = torch.device("cuda:0")
-    torch.cuda.set_device(dev)
+    inst = W.make(wl, with_do=True, with_hidden=bool(wl.hidden) and not args.power)
     n, H, D, blk = inst.n_kept, wl.heads, wl.head_dim, wl.block
     scale = 1.0 / math.sqrt(D)
     nb = -(-n // blk)
+    q, k, v, do = (t.to(dev) for t in (inst.q, inst.k, inst.v, inst.do))
+    if args.power:
+        idx = ut.build_block_index(torch.from_numpy(inst.block_mask).to(dev))
+        res = power_sample(ut, dev, torch.cuda.current_stream(), q, k, v, do, idx, blk, scale)
+        res["workload"] = wl.name
+        print(json.dumps({"power": res}), flush=True)
+        return
 
     # ---- inputs resident in HBM
     mask = torch.from_numpy(inst.fg_mask).to(dev)
     hidden = inst.hidden.to(dev) if inst.hidden is not None else None
     bm = torch.from_numpy(inst.block_mask).to(dev)
-    q, k, v, do = (t.to(dev) for t in (inst.q, inst.k, inst.v, inst.do))
     L = wl.seq_len
     kept = torch.empty(n, dtype=torch.int32, device=dev)
     n_dev = torch.empty(1, dtype=torch.int32, device=dev)
@@ -370,12 +639,16 @@ def main():
         step()
     torch.cuda.synchronize()
     events = [[torch.cuda.Event(enable_timing=True) for _ in range(6)] for _ in range(args.steps)]
+    ut.trace_read()                      # nothing from the warm-up
+    ut.ut_trace_enable(True)             # every launch of the timed steps, on its stream
     torch.cuda.synchronize()
     t0 = time.perf_counter()
     for s in range(args.steps):
         step(events[s])
     torch.cuda.synchronize()
     wall = time.perf_counter() - t0
+    ut.ut_trace_enable(False)
+    trace = ut.trace_read()
     samples = {p: [events[s][i].elapsed_time(events[s][i + 1]) for s in range(args.steps)]
                for i, p in enumerate(phases)}
     per = {p: float(np.mean(x)) for p, x in samples.items()}
@@ -391,6 +664,12 @@ def main():
     bwd_tflops = 2.5 * fwd_flops / (per["bwd"] * 1e-3) / 1e12
     attn_ms = per["fwd"] + per["bwd"]
     copy_bytes = 2 * n * wl.hidden * 2 + 4 * n if hidden is not None else 0
+    kernels = kernel_rooflines(trace, args.steps, fwd_flops, n, H, D, wl.hidden * 2,
+                               wl.name, wl.rho)
+    traced_total = sum(r["total_ms"] for r in trace)
+    for e in kernels:
+        e["share_of_step_kernels"] = round(e.pop("total_ms") / traced_total, 4)
+    dom = max(kernels, key=lambda e: e["share_of_step_kernels"])
 
     result = {
         "metric": "block-sparse attn effective TFLOP/s + ms/layer fwd+bwd at 2K (212,992 tok), % MFMA peak",
@@ -431,24 +710,24 @@ def main():
                  "gbs_gather_rows": round(copy_bytes / ((per["drop"] - ms_compact) * 1e-3) / 1e9, 1)
                  if copy_bytes and per["drop"] > ms_compact else None,
                  "gbs_scatter": round(copy_bytes / (per["scatter"] * 1e-3) / 1e9, 1) if copy_bytes else None},
-        "roofline": {"bound": "mfma", "kernel": "bsattn_fwd_kernel<128,128>",
-                     "achieved": round(fwd_tflops, 2), "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s",
-                     "frac": round(fwd_tflops / PEAK_BF16_TFLOPS, 4),
-                     "traffic": fwd_traffic(wl.name, wl.rho)},
-        # the backward call as a whole (pre-pass, dK/dV and dQ kernels, which
-        # run 7 products per pair for the 5 counted), timed like the forward
-        "roofline_bwd": {"bound": "mfma", "kernels": "bwd_prep_kernel + bwd_dkdv_kernel<128,128> + "
-                                                     "bwd_dq_kernel<128,128>",
-                         "achieved": round(bwd_tflops, 2), "peak": PEAK_BF16_TFLOPS,
-                         "unit": "TFLOP/s", "frac": round(bwd_tflops / PEAK_BF16_TFLOPS, 4)},
+        # the step's dominant kernel (largest share of the traced kernel time)
+        "roofline": {"bound": dom["bound"], "kernel": dom["kernel"], "achieved": dom["achieved"],
+                     "peak": dom["peak"], "unit": dom["unit"], "frac": dom["frac"],
+                     "traffic": dom["traffic"], "ms": dom["ms"], "clock_ghz": dom["clock_ghz"],
+                     "work_per_launch": dom["work_per_launch"]},
+        "kernels": kernels,
+        "trace_ms_per_step": {r["name"]: round(r["total_ms"] / args.steps, 4) for r in trace},
     }
+    if not args.no_sweep:
+        result["sweep"] = sweep(ut, W, dev, stream, {"workload": wl.name, "q": q, "k": k, "v": v,
+                                                     "do": do}, args.sweep_steps)
     result["topk_mask"] = time_topk(ut, q, k, blk, W.kept_off_diagonal(wl.rho, nb), stream)
     result["fg_step"] = time_fg_step(ut, inst.fg_mask, wl.grid, dev, stream)
     result["decode_prep"] = time_decode_prep(ut, inst.fg_mask, wl.grid, dev, stream)
     if not args.no_varlen:
         result["varlen"] = time_varlen(ut, W, dev, stream)
     if not args.no_cpu_baseline:
-        result["cpu_baseline"] = cpu_baseline(inst, args.cpu_seconds)
+        result["cpu_baseline"] = cpu_baseline(inst, args.cpu_seconds, attn_flops)
     print(json.dumps(result), flush=True)
 
 

@@ -65,6 +65,34 @@ const char* ut_last_error(void);
 int ut_abi_version(void);
 
 /* ------------------------------------------------------------------------
+ * Kernel timing (a tracing aid). With tracing on, every kernel the library
+ * launches is bracketed by two HIP events recorded on the stream it runs on;
+ * ut_trace_read waits for those events and returns per-kernel totals in
+ * first-launch order, then forgets them. Off by default. It costs two event
+ * records per launch and is meant for eager launches, not graph capture.
+ *
+ * ut_trace_enable  on != 0 starts recording, 0 stops (records already made
+ *                  stay until read). Always UT_OK.
+ * ut_trace_read    consumes the records made since the last read: fills
+ *                  out[0 .. min(n, max_entries)) and returns n, the number of
+ *                  distinct kernels among them (entries past max_entries are
+ *                  dropped; out may be NULL with max_entries = 0); -1 with
+ *                  ut_last_error() set if an event could not be read (a HIP
+ *                  error).
+ * Names are the kernel's with its head_dim and block where it has them, e.g.
+ * "bsattn_fwd<128,128>", "bwd_dkdv<128,128>", "gather_rows".
+ * ---------------------------------------------------------------------- */
+typedef struct {
+  char name[48];
+  int64_t count;      /* launches recorded */
+  double total_ms;    /* summed durations */
+  double min_ms;
+  double max_ms;
+} ut_kernel_time;
+ut_status ut_trace_enable(int on);
+int ut_trace_read(ut_kernel_time* out, int max_entries);
+
+/* ------------------------------------------------------------------------
  * Background Token Dropping (Sec. 3.2, "Mask Construction and Sequence
  * Compression"): the retained set M_fg of a per-view token-grid foreground
  * mask and the Gather_{M_fg} of a full-sequence hidden state.

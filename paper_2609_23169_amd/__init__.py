@@ -30,7 +30,7 @@ STATUS_NAMES = ["UT_OK", "UT_ERR_INVALID_ARG", "UT_ERR_UNSUPPORTED", "UT_ERR_WOR
 
 # Every symbol the header declares (checked by the CPU test suite).
 EXPORTS = [
-    "ut_last_error", "ut_abi_version",
+    "ut_last_error", "ut_abi_version", "ut_trace_enable", "ut_trace_read",
     "ut_drop_background_workspace_size", "ut_drop_background",
     "ut_scatter_foreground", "ut_build_block_index_workspace_size", "ut_build_block_index",
     "ut_bsattn_fwd", "ut_bsattn_bwd_workspace_size", "ut_bsattn_bwd", "ut_bsattn_bwd_noalloc",
@@ -47,11 +47,19 @@ class UltraTexError(RuntimeError):
         self.status = status
 
 
+class KernelTime(ctypes.Structure):
+    """ut_kernel_time of the C ABI."""
+    _fields_ = [("name", ctypes.c_char * 48), ("count", ctypes.c_int64), ("total_ms", ctypes.c_double),
+                ("min_ms", ctypes.c_double), ("max_ms", ctypes.c_double)]
+
+
 _c = ctypes
 _vp, _i32, _i64, _f32, _sz = _c.c_void_p, _c.c_int32, _c.c_int64, _c.c_float, _c.c_size_t
 _SIGS = {
     "ut_last_error": (_c.c_char_p, []),
     "ut_abi_version": (_c.c_int, []),
+    "ut_trace_enable": (_c.c_int, [_c.c_int]),
+    "ut_trace_read": (_c.c_int, [_c.POINTER(KernelTime), _c.c_int]),
     "ut_drop_background_workspace_size": (_sz, [_i64]),
     "ut_drop_background": (_c.c_int, [_vp, _i64, _vp, _i64, _vp, _i64, _vp, _vp, _vp, _vp, _vp, _sz, _vp]),
     "ut_scatter_foreground": (_c.c_int, [_vp, _vp, _i64, _i64, _vp, _vp]),
@@ -101,6 +109,22 @@ def lib() -> ctypes.CDLL:
 
 def last_error() -> str:
     return lib().ut_last_error().decode()
+
+
+def ut_trace_enable(on: bool) -> int:
+    return lib().ut_trace_enable(1 if on else 0)
+
+
+def trace_read() -> list:
+    """Per-kernel launch timings recorded since the last read (waits for
+    them): [{"name", "count", "total_ms", "min_ms", "max_ms"}, ...]."""
+    cap = 128   # the library launches fewer distinct kernels than this
+    buf = (KernelTime * cap)()
+    n = lib().ut_trace_read(buf, cap)
+    if n < 0:
+        raise UltraTexError("ut_trace_read", UT_ERR_HIP, last_error())
+    return [{"name": k.name.decode(), "count": int(k.count), "total_ms": k.total_ms,
+             "min_ms": k.min_ms, "max_ms": k.max_ms} for k in buf[:min(n, cap)]]
 
 
 def _p(t):

@@ -21,10 +21,11 @@ HERE = os.path.dirname(os.path.abspath(__file__))
 ROOT = os.path.dirname(HERE)
 CSRC = os.path.join(HERE, "csrc")
 OUT = os.path.join(HERE, "libultratex.so")
+DIAG_OUT = os.path.join(HERE, "libutdiag.so")   # measurement aid (include/ultratex_diag.h)
 OBJ = os.path.join(HERE, "_build")
 
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
-SOURCES = ["api.cpp", "btd.hip", "block_index.hip", "bsattn_fwd.hip", "bsattn_bwd.hip",
+SOURCES = ["api.cpp", "trace.cpp", "btd.hip", "block_index.hip", "bsattn_fwd.hip", "bsattn_bwd.hip",
            "topk_mask.hip", "fg_step.hip", "composite.hip"]
 FLAGS = [
     "--offload-arch=gfx950", "-O3", "-std=c++17", "-fPIC",
@@ -57,18 +58,26 @@ SAN_OUT = os.path.join(SAN, "libultratex_sanitize.so")
 SAN_FLAGS = ["-fsanitize=address,undefined", "-fno-omit-frame-pointer", "-fno-sanitize-recover=all"]
 
 
+HOST_SOURCES = ["api.cpp", "trace.cpp"]   # no device code: g++ builds them for the sanitizers
+
+
 def build_sanitized(objs, verbose: bool = False) -> str:
-    """api.cpp through g++ with ASan + UBSan, linked with the HIP objects."""
+    """The host sources through g++ with ASan + UBSan, linked with the HIP
+    kernel objects."""
     os.makedirs(SAN, exist_ok=True)
-    api_obj = os.path.join(SAN, "api.o")
-    cmd = [GXX, "-std=c++17", "-O1", "-g", "-fPIC", "-Wall", *SAN_FLAGS,
-           "-D__HIP_PLATFORM_AMD__", "-I/opt/rocm/include", "-I", os.path.join(ROOT, "include"),
-           "-I", CSRC, "-c", os.path.join(CSRC, "api.cpp"), "-o", api_obj]
-    r = subprocess.run(cmd, capture_output=True, text=True)
-    if r.returncode != 0:
-        raise RuntimeError(f"g++ (sanitized api.cpp) failed:\n{r.stdout}{r.stderr}")
-    kernels = [o for o in objs if os.path.basename(o) != "api.o"]
-    cmd = [GXX, "-shared", *SAN_FLAGS, api_obj, *kernels, "-L/opt/rocm/lib", "-lamdhip64",
+    host_objs = []
+    for src in HOST_SOURCES:
+        obj = os.path.join(SAN, os.path.splitext(src)[0] + ".o")
+        cmd = [GXX, "-std=c++17", "-O1", "-g", "-fPIC", "-Wall", *SAN_FLAGS,
+               "-D__HIP_PLATFORM_AMD__", "-I/opt/rocm/include", "-I", os.path.join(ROOT, "include"),
+               "-I", CSRC, "-c", os.path.join(CSRC, src), "-o", obj]
+        r = subprocess.run(cmd, capture_output=True, text=True)
+        if r.returncode != 0:
+            raise RuntimeError(f"g++ (sanitized {src}) failed:\n{r.stdout}{r.stderr}")
+        host_objs.append(obj)
+    host = {os.path.splitext(s)[0] + ".o" for s in HOST_SOURCES}
+    kernels = [o for o in objs if os.path.basename(o) not in host]
+    cmd = [GXX, "-shared", *SAN_FLAGS, *host_objs, *kernels, "-L/opt/rocm/lib", "-lamdhip64",
            "-Wl,-rpath,/opt/rocm/lib", "-o", SAN_OUT]
     r = subprocess.run(cmd, capture_output=True, text=True)
     if r.returncode != 0:
@@ -90,6 +99,14 @@ def build(verbose: bool = False, sanitize: bool = False) -> str:
     os.replace(tmp, OUT)
     if verbose:
         print(f"built {OUT}")
+    dobj = _compile("diag_mfma.hip")
+    r = subprocess.run([HIPCC, "--offload-arch=gfx950", "-shared", "-fPIC", dobj, "-o", DIAG_OUT + ".tmp"],
+                       capture_output=True, text=True)
+    if r.returncode != 0:
+        raise RuntimeError(f"link of the diagnostic library failed:\n{r.stdout}{r.stderr}")
+    os.replace(DIAG_OUT + ".tmp", DIAG_OUT)
+    if verbose:
+        print(f"built {DIAG_OUT}")
     if sanitize or os.environ.get("UT_SANITIZE", "0") not in ("", "0"):
         build_sanitized(objs, verbose)
     return OUT

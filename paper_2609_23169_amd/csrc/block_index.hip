@@ -135,16 +135,31 @@ hipError_t launch_block_index(const uint8_t* mask, int B, int H, int Nq, int Nk,
   const int64_t rows = (int64_t)B * H * Nq;
   const unsigned row_blocks = (unsigned)((rows + 3) / 4);
   const dim3 col_grid((unsigned)((Nk + 63) / 64), (unsigned)(B * H));
-  hipLaunchKernelGGL(rows_pass<false>, dim3(row_blocks), dim3(kThreads), 0, s, mask, rows, Nk,
+  {
+    TraceScope ts_(s, "rows_pass_count");
+    hipLaunchKernelGGL(rows_pass<false>, dim3(row_blocks), dim3(kThreads), 0, s, mask, rows, Nk,
                      q_rowptr, q_cols, cap);
-  hipLaunchKernelGGL(cols_pass<false>, col_grid, dim3(kThreads), 0, s, mask, Nq, Nk, kv_colptr,
+  }
+  {
+    TraceScope ts_(s, "cols_pass_count");
+    hipLaunchKernelGGL(cols_pass<false>, col_grid, dim3(kThreads), 0, s, mask, Nq, Nk, kv_colptr,
                      kv_rows, cap);
-  hipLaunchKernelGGL(scan_counts, dim3(2), dim3(1024), 0, s, q_rowptr, rows, kv_colptr,
+  }
+  {
+    TraceScope ts_(s, "scan_counts");
+    hipLaunchKernelGGL(scan_counts, dim3(2), dim3(1024), 0, s, q_rowptr, rows, kv_colptr,
                      (int64_t)B * H * Nk);
-  hipLaunchKernelGGL(rows_pass<true>, dim3(row_blocks), dim3(kThreads), 0, s, mask, rows, Nk,
+  }
+  {
+    TraceScope ts_(s, "rows_pass_fill");
+    hipLaunchKernelGGL(rows_pass<true>, dim3(row_blocks), dim3(kThreads), 0, s, mask, rows, Nk,
                      q_rowptr, q_cols, cap);
-  hipLaunchKernelGGL(cols_pass<true>, col_grid, dim3(kThreads), 0, s, mask, Nq, Nk, kv_colptr,
+  }
+  {
+    TraceScope ts_(s, "cols_pass_fill");
+    hipLaunchKernelGGL(cols_pass<true>, col_grid, dim3(kThreads), 0, s, mask, Nq, Nk, kv_colptr,
                      kv_rows, cap);
+  }
   return hipGetLastError();
 }
 

@@ -451,20 +451,29 @@ hipError_t launch_bwd_t(const void* q, const void* k, const void* v, const void*
   auto bf = [](const void* p) { return static_cast<const __bf16*>(p); };
   float* aux = ws;
   const int64_t rows_total = sh.T * sh.H * (D / 8);
-  hipLaunchKernelGGL((bwd_prep_kernel<D>), dim3((unsigned)((rows_total + 255) / 256)), dim3(256), 0,
+  {
+    TraceScope ts_(s, "bwd_prep", D);
+    hipLaunchKernelGGL((bwd_prep_kernel<D>), dim3((unsigned)((rows_total + 255) / 256)), dim3(256), 0,
                      s, bf(o), bf(dout), lse, aux, sh.T, sh.N, sh.H, sh.cu != nullptr);
+  }
   // One workgroup per (b, h, block) in plain order. Workgroups go round-robin
   // to the 8 XCDs, so all XCDs work on the same few heads at once (their K and
   // V stay in the shared last-level cache) and a run of heavy blocks is spread
   // over every XCD.
   const dim3 grid((unsigned)((int64_t)sh.B * sh.H * sh.nblk));
-  hipLaunchKernelGGL((bwd_dkdv_kernel<D, BLOCK>), grid, dim3(64 * (BLOCK / 32)), 0, s,
+  {
+    TraceScope ts_(s, "bwd_dkdv", D, BLOCK);
+    hipLaunchKernelGGL((bwd_dkdv_kernel<D, BLOCK>), grid, dim3(64 * (BLOCK / 32)), 0, s,
                      bf(q), bf(k), bf(v), bf(dout), aux, static_cast<__bf16*>(dk),
                      static_cast<__bf16*>(dv), sh.B, sh.N, sh.H, sh.nblk, sh.scale, colptr, rows,
                      sh.cu, sh.T);
-  hipLaunchKernelGGL((bwd_dq_kernel<D, BLOCK>), grid, dim3(64 * (BLOCK / 32)), 0, s,
+  }
+  {
+    TraceScope ts_(s, "bwd_dq", D, BLOCK);
+    hipLaunchKernelGGL((bwd_dq_kernel<D, BLOCK>), grid, dim3(64 * (BLOCK / 32)), 0, s,
                      bf(q), bf(k), bf(v), bf(dout), aux, static_cast<__bf16*>(dq), sh.B, sh.N, sh.H,
                      sh.nblk, sh.scale, rowptr, cols, sh.cu, sh.T);
+  }
   return hipGetLastError();
 }
 

@@ -370,10 +370,13 @@ hipError_t launch_fwd_t(const void* q, const void* k, const void* v, void* o, fl
   // V stay in the shared last-level cache) and a run of heavy blocks is spread
   // over every XCD.
   const dim3 grid((unsigned)((int64_t)sh.B * sh.H * sh.nblk));
-  hipLaunchKernelGGL((bsattn_fwd_kernel<D, BLOCK>), grid, dim3(FwdCfg<D, BLOCK>::NT), 0,
+  {
+    TraceScope ts_(s, "bsattn_fwd", D, BLOCK);
+    hipLaunchKernelGGL((bsattn_fwd_kernel<D, BLOCK>), grid, dim3(FwdCfg<D, BLOCK>::NT), 0,
                      s, static_cast<const __bf16*>(q), static_cast<const __bf16*>(k),
                      static_cast<const __bf16*>(v), static_cast<__bf16*>(o), lse, sh.B, sh.N, sh.H,
                      sh.nblk, sh.scale, rowptr, cols, sh.cu, sh.T);
+  }
   return hipGetLastError();
 }
 

@@ -162,10 +162,19 @@ hipError_t launch_compact(const uint8_t* mask, int64_t L, int64_t capacity, int3
                           int32_t* inv_idx, int32_t* n_kept, int32_t* tile_scratch,
                           hipStream_t s) {
   const int64_t nt = compact_tiles(L);
-  hipLaunchKernelGGL(compact_count, dim3((unsigned)nt), dim3(kThreads), 0, s, mask, L, tile_scratch);
-  hipLaunchKernelGGL(compact_scan, dim3(1), dim3(kThreads), 0, s, tile_scratch, nt, n_kept);
-  hipLaunchKernelGGL(compact_fill, dim3((unsigned)nt), dim3(kThreads), 0, s, mask, L, tile_scratch,
+  {
+    TraceScope ts_(s, "compact_count");
+    hipLaunchKernelGGL(compact_count, dim3((unsigned)nt), dim3(kThreads), 0, s, mask, L, tile_scratch);
+  }
+  {
+    TraceScope ts_(s, "compact_scan");
+    hipLaunchKernelGGL(compact_scan, dim3(1), dim3(kThreads), 0, s, tile_scratch, nt, n_kept);
+  }
+  {
+    TraceScope ts_(s, "compact_fill");
+    hipLaunchKernelGGL(compact_fill, dim3((unsigned)nt), dim3(kThreads), 0, s, mask, L, tile_scratch,
                      capacity, kept_idx, inv_idx);
+  }
   return hipGetLastError();
 }
 
@@ -174,9 +183,12 @@ hipError_t launch_gather(const void* x_full, int64_t row_bytes, void* x_packed, 
   if (capacity == 0) return hipSuccess;
   const int64_t rows = min(capacity, kGatherRowsPerPass);
   const int64_t blocks = (rows + kRowsPerBlock - 1) / kRowsPerBlock;
-  hipLaunchKernelGGL(gather_rows, dim3((unsigned)blocks), dim3(kThreads), 0, s,
+  {
+    TraceScope ts_(s, "gather_rows");
+    hipLaunchKernelGGL(gather_rows, dim3((unsigned)blocks), dim3(kThreads), 0, s,
                      static_cast<const u32x4*>(x_full), row_bytes / 16,
                      static_cast<u32x4*>(x_packed), capacity, kept_idx, n_kept);
+  }
   return hipGetLastError();
 }
 
@@ -184,9 +196,12 @@ hipError_t launch_scatter(const void* x_packed, const int32_t* kept_idx, int64_t
                           int64_t row_bytes, void* x_full, hipStream_t s) {
   if (n_kept == 0) return hipSuccess;
   const int64_t blocks = (n_kept + kRowsPerBlock - 1) / kRowsPerBlock;
-  hipLaunchKernelGGL(scatter_rows, dim3((unsigned)blocks), dim3(kThreads), 0, s,
+  {
+    TraceScope ts_(s, "scatter_rows");
+    hipLaunchKernelGGL(scatter_rows, dim3((unsigned)blocks), dim3(kThreads), 0, s,
                      static_cast<const u32x4*>(x_packed), row_bytes / 16,
                      static_cast<u32x4*>(x_full), n_kept, kept_idx);
+  }
   return hipGetLastError();
 }
 

@@ -15,6 +15,21 @@ ut_status fail(ut_status st, const char* fmt, ...);
 // Maps a HIP error (if any) to UT_ERR_HIP with context; UT_OK otherwise.
 ut_status check_hip(hipError_t e, const char* what);
 
+// Brackets the kernel launches of its lifetime with HIP events on `s` while
+// tracing is on (ut_trace_enable); name base<a,b> (a, b < 0: omitted).
+class TraceScope {
+ public:
+  TraceScope(hipStream_t s, const char* base, int a = -1, int b = -1);
+  ~TraceScope();
+  TraceScope(const TraceScope&) = delete;
+  TraceScope& operator=(const TraceScope&) = delete;
+
+ private:
+  hipStream_t stream_;
+  hipEvent_t start_ = nullptr;
+  char name_[48] = "";
+};
+
 // Host checks of the validate mode, on host copies of the arguments.
 // Compressed lists: ptr[0] = 0, ptr non-decreasing, ptr[rows] = n_idx, and
 // every row strictly ascending within [0, limit). With idx = NULL only the

@@ -93,9 +93,12 @@ hipError_t launch_composite(const void* packed, int64_t n_kept, const int32_t* i
                             const void* bg, int64_t bg_rows, int64_t row_bytes, void* out,
                             hipStream_t s) {
   const int64_t cpr = row_bytes / 16;
-  hipLaunchKernelGGL(composite_kernel, dim3(grid_of(L * cpr)), dim3(kThreads), 0, s,
+  {
+    TraceScope ts_(s, "composite");
+    hipLaunchKernelGGL(composite_kernel, dim3(grid_of(L * cpr)), dim3(kThreads), 0, s,
                      static_cast<const u32x4_t*>(packed), n_kept, inv, L,
                      static_cast<const u32x4_t*>(bg), bg_rows, cpr, static_cast<u32x4_t*>(out));
+  }
   return hipGetLastError();
 }
 
@@ -103,12 +106,18 @@ hipError_t launch_token_mask(const uint8_t* alpha, int V, int Hp, int Wp, int pa
                              int radius, uint8_t* out, uint8_t* pooled, hipStream_t s) {
   const int gh = Hp / patch, gw = Wp / patch;
   const int64_t tokens = (int64_t)V * gh * gw;
-  hipLaunchKernelGGL(mask_pool_kernel, dim3(grid_of(tokens)), dim3(kThreads), 0, s, alpha, V, Hp,
+  {
+    TraceScope ts_(s, "mask_pool");
+    hipLaunchKernelGGL(mask_pool_kernel, dim3(grid_of(tokens)), dim3(kThreads), 0, s, alpha, V, Hp,
                      Wp, patch, (uint32_t)thr, radius > 0 ? pooled : out);
+  }
   hipError_t e = hipGetLastError();
   if (e != hipSuccess || radius == 0) return e;
-  hipLaunchKernelGGL(mask_dilate_kernel, dim3(grid_of(tokens)), dim3(kThreads), 0, s, pooled, V,
+  {
+    TraceScope ts_(s, "mask_dilate");
+    hipLaunchKernelGGL(mask_dilate_kernel, dim3(grid_of(tokens)), dim3(kThreads), 0, s, pooled, V,
                      gh, gw, radius, out);
+  }
   return hipGetLastError();
 }
 

@@ -122,6 +122,7 @@ hipError_t launch_euler_fg(float* z, int64_t L, int64_t C, const void* v, bool v
                            const int32_t* kept, int64_t n, float dt, hipStream_t s) {
   if (n == 0) return hipSuccess;
   const int grid = grid_for(n * (C / 4));
+  TraceScope ts_(s, "euler");
   if (v_bf16)
     hipLaunchKernelGGL(euler_kernel<__bf16>, dim3(grid), dim3(kThreads), 0, s, z,
                        static_cast<const __bf16*>(v), kept, n, L, (int)C, dt);
@@ -140,14 +141,20 @@ hipError_t launch_fg_loss(const void* v, bool v_bf16, const void* eps, const voi
   hipLaunchKernelGGL((loss_partial_kernel<VT, XT>), dim3(grid), dim3(kThreads), 0, s,        \
                      static_cast<const VT*>(v), static_cast<const XT*>(eps),                 \
                      static_cast<const XT*>(z0), kept, n, L, c, grad, partial)
-  if (v_bf16 && x_bf16) UT_LOSS(__bf16, __bf16);
-  else if (v_bf16) UT_LOSS(__bf16, float);
-  else if (x_bf16) UT_LOSS(float, __bf16);
-  else UT_LOSS(float, float);
+  {
+    TraceScope ts_(s, "loss_partial");
+    if (v_bf16 && x_bf16) UT_LOSS(__bf16, __bf16);
+    else if (v_bf16) UT_LOSS(__bf16, float);
+    else if (x_bf16) UT_LOSS(float, __bf16);
+    else UT_LOSS(float, float);
+  }
 #undef UT_LOSS
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
-  hipLaunchKernelGGL(loss_final_kernel, dim3(1), dim3(64), 0, s, partial, grid, n, c, loss);
+  {
+    TraceScope ts_(s, "loss_final");
+    hipLaunchKernelGGL(loss_final_kernel, dim3(1), dim3(64), 0, s, partial, grid, n, c, loss);
+  }
   return hipGetLastError();
 }
 

@@ -252,8 +252,11 @@ hipError_t launch_select(const float* pq, const float* pk, uint8_t* mask, int B,
                          int nq, int k_keep, int prefix, hipStream_t s) {
   const int groups = (nq + QR - 1) / QR;
   const size_t lds = (size_t)QR * (D + nq) * sizeof(float);
-  hipLaunchKernelGGL((select_kernel<QR>), dim3((unsigned)((int64_t)B * H * groups)),
+  {
+    TraceScope ts_(s, "topk_select", QR);
+    hipLaunchKernelGGL((select_kernel<QR>), dim3((unsigned)((int64_t)B * H * groups)),
                      dim3(kSelThreads), lds, s, pq, pk, mask, D, nq, nq, k_keep, prefix);
+  }
   return hipGetLastError();
 }
 
@@ -261,9 +264,12 @@ template <int D>
 hipError_t launch_select_mfma(const float* pq, const float* pk, uint8_t* mask, int B, int H,
                               int nq, int k_keep, int prefix, hipStream_t s) {
   const int groups = (nq + 15) / 16;
-  hipLaunchKernelGGL((select_mfma_kernel<D>), dim3((unsigned)((int64_t)B * H * groups)),
+  {
+    TraceScope ts_(s, "topk_select_mfma", D);
+    hipLaunchKernelGGL((select_mfma_kernel<D>), dim3((unsigned)((int64_t)B * H * groups)),
                      dim3(kSelMfmaThreads), (size_t)16 * nq * sizeof(uint32_t), s, pq, pk, mask, nq,
                      nq, k_keep, prefix);
+  }
   return hipGetLastError();
 }
 
@@ -285,9 +291,12 @@ hipError_t launch_topk_block_mask(const void* q, const void* k, int B, int N, in
   // one 16-byte chunk of a token row per thread (up to 1024 threads)
   const int chunks = H * D / 8;
   const int pool_threads = (int)std::min<int64_t>(kPoolMaxThreads, (chunks + 63) / 64 * 64);
-  hipLaunchKernelGGL(pool_kernel, dim3((unsigned)nblk, (unsigned)B, 2), dim3(pool_threads), 0, s,
+  {
+    TraceScope ts_(s, "topk_pool");
+    hipLaunchKernelGGL(pool_kernel, dim3((unsigned)nblk, (unsigned)B, 2), dim3(pool_threads), 0, s,
                      static_cast<const __bf16*>(q), static_cast<const __bf16*>(k), pq, pk, N, H,
                      D, block, nblk);
+  }
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
   if ((D == 64 || D == 128) && 16 * (int64_t)(D + nblk) * 4 <= kTopkMaxLds)

@@ -31,6 +31,28 @@ def test_library_exports_every_declared_symbol():
     assert lib.ut_abi_version() == 2
 
 
+def test_trace_switch_and_empty_read():
+    lib = ut.lib()
+    assert lib.ut_trace_enable(1) == ut.UT_OK
+    assert lib.ut_trace_enable(0) == ut.UT_OK
+    assert ut.trace_read() == []          # nothing launched on this host
+    assert lib.ut_trace_read(None, 0) == 0
+
+
+def test_diag_library_exports_its_header():
+    diag = os.path.join(os.path.dirname(HEADER), "ultratex_diag.h")
+    names = sorted(set(re.findall(r"\b(ut_[a-z_0-9]+)\s*\(", open(diag).read())))
+    assert names == ["ut_diag_mfma_rate"]
+    lib = ctypes.CDLL(os.path.join(os.path.dirname(ut.__file__), "libutdiag.so"))
+    for n in names:
+        assert hasattr(lib, n), n
+    f = lib.ut_diag_mfma_rate
+    f.argtypes = [ctypes.c_int] * 3 + [ctypes.c_void_p] * 4
+    assert f(2, 10, 4, FAKE, FAKE, FAKE, None) == -1       # unknown shape: nothing launched
+    assert f(0, 0, 4, FAKE, FAKE, FAKE, None) == -1
+    assert f(1, 10, 4, None, FAKE, FAKE, None) == -1
+
+
 def test_workspace_sizes():
     assert ut.ut_drop_background_workspace_size(212992) == 52 * 4
     assert ut.ut_drop_background_workspace_size(1) == 4
