@@ -7,14 +7,19 @@
 //   dQ    : one workgroup per (b, h, query block i), walking S_i (row lists).
 //           Each wave owns 32 queries, with its Q and dO rows as MFMA operands
 //           in registers. Per 64-key tile streamed through LDS:
-//           S^T = K Q^T and dP^T = V dO^T (lane = query column),
-//           P = exp(S - LSE), dS^T = P^T o (dP^T - delta), dQ^T += K^T dS^T;
+//           S^T = K Q^T and dP^T = V dO^T (lane = query column, 32x32x16),
+//           P = exp(S - LSE), dS^T = P^T o (dP^T - delta), then
+//           dQ^T += K^T dS^T on 16x16x32 MFMA after one v_permlane16_swap per
+//           register moves dS^T to the B-operand layout (as the forward does
+//           for P; the smaller shape draws less power per FLOP);
 //   dK/dV : one workgroup per (b, h, key block j), walking the query blocks
 //           that select j (column lists) in 32-row query tiles. One wave per
 //           32 keys (K rows in registers, the key block's V rows in LDS):
-//           S = Q K^T and dP = dO V^T (lane = key column; the dP accumulator
-//           starts at -delta, so it ends as dP - delta), dV^T += dO^T P and
-//           dK^T += Q^T dS with transposing LDS reads. Two workgroups share a
+//           S = Q K^T and dP = dO V^T (lane = key column, 32x32x16; the dP
+//           accumulator starts at -delta, so it ends as dP - delta), then
+//           dV^T += dO^T P and dK^T += Q^T dS on 16x16x32 after a
+//           v_permlane16_swap exchange of P and dS, with transposing LDS
+//           reads. Two workgroups share a
 //           CU, so the two waves on each SIMD belong to different workgroups
 //           and never wait at the same barrier.
 //
@@ -145,9 +150,13 @@ __global__ __launch_bounds__(64 * (BLOCK / 32), (BLOCK == 128 || D == 64) ? 2 : 
   while (p1 > p0 && cols[p1 - 1] >= (N + BLOCK - 1) / BLOCK) --p1;   // past the sample
   const int T = (p1 - p0) * C::SUBS;
 
-  f32x16 dqt[C::DT];
+  // dQ^T in the 16x16 layout: dq16[dt][qg] lane holds
+  // dQ^T[16 dt + 4 gq + (0..3)][query 32 w + 16 qg + c16]
+  constexpr int DT16 = D / 16;
+  const int c16 = lane & 15, gq = lane >> 4;
+  f32x4 dq16[DT16][2];
 #pragma unroll
-  for (int dt = 0; dt < C::DT; ++dt) dqt[dt] = f32x16{};
+  for (int dt = 0; dt < DT16; ++dt) dq16[dt][0] = dq16[dt][1] = f32x4{};
 
   if (T > 0) {
     bf16x8 qop[C::KS], doop[C::KS];
@@ -162,6 +171,17 @@ __global__ __launch_bounds__(64 * (BLOCK / 32), (BLOCK == 128 || D == 64) ? 2 : 
     const int64_t ar = sr.stat0 + min(q, N - 1);
     const float lse2 = aux[ar], ndl = aux[(int64_t)H * T_tok + ar];   // LSE log2 e, -delta
     const LaneOffsets<C> lo(w, lane, tok_stride);
+    // K^T operand of the 16x16x32 dQ product for d tile dt, key step kc:
+    // lane group gq reads key rows 32 kc + base(gq) + (c16 >> 2) (slots
+    // 0..3) and the same + 16 (slots 4..7), columns 16 dt + 4 (c16 & 3) .. +3,
+    // base(gq) = 8 (gq & 1) + 4 (gq >> 1): the keys the dS exchange leaves in
+    // that lane group.
+    int ktr[DT16];
+#pragma unroll
+    for (int dt = 0; dt < DT16; ++dt) {
+      const int d = 16 * dt + 4 * (c16 & 3);
+      ktr[dt] = lds_off<C::CPR>(8 * (gq & 1) + 4 * (gq >> 1) + (c16 >> 2), d >> 3) + 2 * (d & 7);
+    }
 
     auto load_tile = [&](const __bf16* X, int t, char* dst) __attribute__((always_inline)) {
       const int j = cols[p0 + t / C::SUBS];
@@ -173,47 +193,60 @@ __global__ __launch_bounds__(64 * (BLOCK / 32), (BLOCK == 128 || D == 64) ? 2 : 
     };
     const float c2 = scale * kLog2e;
 
+    // One 64-key tile as two 32-key halves kt: S^T and dP^T (32x32x16), dS^T,
+    // its exchange to the 16x16 B-operand layout, and the dQ product of that
+    // half (16x16x32); only one half's score accumulators are live at a time.
     auto step = [&](int t, const char* kt_lds, const char* vt_lds, auto masked)
         __attribute__((always_inline)) {
-      f32x16 s[2] = {f32x16{}, f32x16{}}, dp[2] = {f32x16{}, f32x16{}};
-#pragma unroll
-      for (int ks = 0; ks < C::KS; ++ks)
-#pragma unroll
-        for (int kt = 0; kt < 2; ++kt) {
-          const int off = lo.row[ks] + kt * 32 * C::ROWB;
-          s[kt] = mfma32(*reinterpret_cast<const bf16x8*>(kt_lds + off), qop[ks], s[kt]);
-          dp[kt] = mfma32(*reinterpret_cast<const bf16x8*>(vt_lds + off), doop[ks], dp[kt]);
-        }
-      int lim = C::ST;
+      int lim = 2 * C::ST;
       if constexpr (decltype(masked)::value) {   // keys past N in a short last block
         const int j = cols[p0 + t / C::SUBS];
         lim = N - (j * BLOCK + (t % C::SUBS) * C::ST);
       }
-      bf16x8 dsb[2][2];
-      __builtin_amdgcn_sched_barrier(0);   // keep the dQ operand reads below (register pressure)
 #pragma unroll
-      for (int kt = 0; kt < 2; ++kt)
+      for (int kt = 0; kt < 2; ++kt) {
+        f32x16 s = f32x16{}, dp = f32x16{};
 #pragma unroll
-        for (int e = 0; e < 16; ++e) {
-          float p = fast_exp2(__builtin_fmaf(s[kt][e], c2, -lse2));
-          if constexpr (decltype(masked)::value)
-            p = 32 * kt + 8 * (e >> 2) + 4 * g + (e & 3) >= lim ? 0.f : p;
-          dsb[kt][e >> 3][e & 7] = (__bf16)(p * (dp[kt][e] + ndl));
+        for (int ks = 0; ks < C::KS; ++ks) {
+          const int off = lo.row[ks] + kt * 32 * C::ROWB;
+          s = mfma32(*reinterpret_cast<const bf16x8*>(kt_lds + off), qop[ks], s);
+          dp = mfma32(*reinterpret_cast<const bf16x8*>(vt_lds + off), doop[ks], dp);
         }
-      __builtin_amdgcn_sched_barrier(0);
-      // dQ^T += K^T dS^T: K^T tile kt, half hh covers keys 32kt + 16hh + {4g+0..3, 8+4g+0..3}
+        // dS^T as bf16 pairs: pq[0] holds elements 0-3, 8-11 (keys
+        // 32 kt + 4 g + {0..3, 16..19}), pq[1] elements 4-7, 12-15
+        u32x4 pq[2];
 #pragma unroll
-      for (int dt = 0; dt < C::DT; ++dt)
-#pragma unroll
-        for (int kt = 0; kt < 2; ++kt)
-#pragma unroll
-          for (int hh = 0; hh < 2; ++hh) {
-            const char* kb = kt_lds + (32 * kt + 16 * hh) * C::ROWB;
-            const s16x4 l4 = lds_read_tr16(kb + lo.tr[dt][0]);
-            const s16x4 h4 = lds_read_tr16(kb + lo.tr[dt][1]);
-            const s16x8 k8 = {l4[0], l4[1], l4[2], l4[3], h4[0], h4[1], h4[2], h4[3]};
-            dqt[dt] = mfma32(__builtin_bit_cast(bf16x8, k8), dsb[kt][hh], dqt[dt]);
+        for (int e = 0; e < 16; e += 2) {
+          float p0 = fast_exp2(__builtin_fmaf(s[e], c2, -lse2));
+          float p1 = fast_exp2(__builtin_fmaf(s[e + 1], c2, -lse2));
+          if constexpr (decltype(masked)::value) {
+            const int key = 32 * kt + 8 * (e >> 2) + 4 * g + (e & 3);
+            p0 = key >= lim ? 0.f : p0;
+            p1 = key + 1 >= lim ? 0.f : p1;
           }
+          pq[(e >> 2) & 1][((e & 3) >> 1) + 2 * (e >> 3)] =
+              pack_bf16x2(p0 * (dp[e] + ndl), p1 * (dp[e + 1] + ndl));
+        }
+        // to the B-operand layout of two 16-query groups (as the forward
+        // does for P): register 0 serves queries c16, register 1 16 + c16
+#pragma unroll
+        for (int v = 0; v < 4; ++v) {
+          const auto r = __builtin_amdgcn_permlane16_swap(pq[0][v], pq[1][v], false, false);
+          pq[0][v] = r[0];
+          pq[1][v] = r[1];
+        }
+        // dQ^T += K^T dS^T over this half's 32 keys
+#pragma unroll
+        for (int dt = 0; dt < DT16; ++dt) {
+          const char* kb = kt_lds + 32 * kt * C::ROWB + ktr[dt];
+          const s16x4 l4 = lds_read_tr16(kb);
+          const s16x4 h4 = lds_read_tr16(kb + 16 * C::ROWB);
+          const s16x8 k8 = {l4[0], l4[1], l4[2], l4[3], h4[0], h4[1], h4[2], h4[3]};
+          const bf16x8 av = __builtin_bit_cast(bf16x8, k8);
+          dq16[dt][0] = mfma16(av, __builtin_bit_cast(bf16x8, pq[0]), dq16[dt][0]);
+          dq16[dt][1] = mfma16(av, __builtin_bit_cast(bf16x8, pq[1]), dq16[dt][1]);
+        }
+      }
     };
     auto iter = [&](int t, auto par, auto masked) __attribute__((always_inline)) {
       constexpr int P = decltype(par)::value;
@@ -255,17 +288,18 @@ __global__ __launch_bounds__(64 * (BLOCK / 32), (BLOCK == 128 || D == 64) ? 2 : 
     }
   }
 
-  if (q < N) {
-    const int64_t off = base_bh + (int64_t)q * tok_stride;
 #pragma unroll
-    for (int dt = 0; dt < C::DT; ++dt)
+  for (int qg = 0; qg < 2; ++qg) {
+    const int qo = i * BLOCK + 32 * w + 16 * qg + c16;
+    if (qo >= N) continue;
+    const int64_t off = base_bh + (int64_t)qo * tok_stride;
 #pragma unroll
-      for (int e4 = 0; e4 < 4; ++e4) {
-        bf16x4 v4;
+    for (int dt = 0; dt < DT16; ++dt) {
+      bf16x4 v4;
 #pragma unroll
-        for (int e = 0; e < 4; ++e) v4[e] = (__bf16)(dqt[dt][4 * e4 + e] * scale);
-        *reinterpret_cast<bf16x4*>(dQ + off + 32 * dt + 8 * e4 + 4 * g) = v4;
-      }
+      for (int e = 0; e < 4; ++e) v4[e] = (__bf16)(dq16[dt][qg][e] * scale);
+      *reinterpret_cast<bf16x4*>(dQ + off + 16 * dt + 4 * gq) = v4;
+    }
   }
 }
 
@@ -311,9 +345,13 @@ __global__ __launch_bounds__(64 * (BLOCK / 32), 256 / BLOCK) void bwd_dkdv_kerne
   while (p1 > p0 && rows_list[p1 - 1] >= (N + BLOCK - 1) / BLOCK) --p1;   // past the sample
   const int T = (p1 - p0) * C::SUBS;
 
-  f32x16 dkt[C::DT], dvt[C::DT];
+  // dK^T and dV^T in the 16x16 layout: [dt][kg] lane holds
+  // X^T[16 dt + 4 gq + (0..3)][key 32 kw + 16 kg + c16]
+  constexpr int DT16 = D / 16;
+  const int c16 = lane & 15, gq = lane >> 4;
+  f32x4 dk16[DT16][2], dv16[DT16][2];
 #pragma unroll
-  for (int dt = 0; dt < C::DT; ++dt) dkt[dt] = dvt[dt] = f32x16{};
+  for (int dt = 0; dt < DT16; ++dt) dk16[dt][0] = dk16[dt][1] = dv16[dt][0] = dv16[dt][1] = f32x4{};
 
   if (T > 0) {
     bf16x8 kop[C::KS];
@@ -335,6 +373,16 @@ __global__ __launch_bounds__(64 * (BLOCK / 32), 256 / BLOCK) void bwd_dkdv_kerne
                             lo.dma[u] + half * C::ST * (int)(tok_stride * 2));
     }
     const char* const vrow = vblk_lds + 32 * kw * C::ROWB;   // this wave's 32 keys
+    // dO^T and Q^T operands of the 16x16x32 products for d tile dt: lane group
+    // gq reads query rows base(gq) + (c16 >> 2) (slots 0..3) and the same + 16
+    // (slots 4..7), columns 16 dt + 4 (c16 & 3) .. +3, base(gq) =
+    // 8 (gq & 1) + 4 (gq >> 1): the rows the P / dS exchange leaves there.
+    int rtr[DT16];
+#pragma unroll
+    for (int dt = 0; dt < DT16; ++dt) {
+      const int d = 16 * dt + 4 * (c16 & 3);
+      rtr[dt] = lds_off<C::CPR>(8 * (gq & 1) + 4 * (gq >> 1) + (c16 >> 2), d >> 3) + 2 * (d & 7);
+    }
 
     // Tile t: 32 query rows of Q and dO, and their {LSE log2 e, -delta}.
     auto load_tile = [&](int t, char* qd, char* od, char* ad) __attribute__((always_inline)) {
@@ -375,35 +423,50 @@ __global__ __launch_bounds__(64 * (BLOCK / 32), 256 / BLOCK) void bwd_dkdv_kerne
         const bf16x8 vop = *reinterpret_cast<const bf16x8*>(vrow + lo.row[ks]);
         dp = mfma32(*reinterpret_cast<const bf16x8*>(ot_lds + off), vop, dp);
       }
-      // rows 8 a + 4 g + (0..3): P and dS, as the B operands of the
-      // second products (half hh: rows 16 hh + {4g+0..3, 8+4g+0..3})
-      bf16x8 pb[2], dsb[2];
+      // P and dS (query rows 8 a + 4 g + (0..3) of key column l32) as bf16
+      // pairs: [0] holds elements 0-3, 8-11 (rows 4 g + {0..3, 16..19}),
+      // [1] elements 4-7, 12-15 (rows 4 g + {8..11, 24..27})
+      u32x4 pp[2], pd[2];
 #pragma unroll
       for (int a = 0; a < 4; ++a) {
         const f32x4 ls = *reinterpret_cast<const f32x4*>(a_pl + 8 * a);
 #pragma unroll
-        for (int e = 0; e < 4; ++e) {
+        for (int e = 0; e < 4; e += 2) {
           const int idx = 4 * a + e;
-          const float p = fast_exp2(__builtin_fmaf(s[idx], c2, -ls[e]));
-          pb[idx >> 3][idx & 7] = (__bf16)p;
-          dsb[idx >> 3][idx & 7] = (__bf16)(p * dp[idx]);
+          const float p0 = fast_exp2(__builtin_fmaf(s[idx], c2, -ls[e]));
+          const float p1 = fast_exp2(__builtin_fmaf(s[idx + 1], c2, -ls[e + 1]));
+          const int r = (idx >> 2) & 1, c = ((idx & 3) >> 1) + 2 * (idx >> 3);
+          pp[r][c] = pack_bf16x2(p0, p1);
+          pd[r][c] = pack_bf16x2(p0 * dp[idx], p1 * dp[idx + 1]);
         }
+      }
+      // to the B-operand layout of two 16-key groups: register 0 serves keys
+      // c16 of this wave's 32, register 1 keys 16 + c16
+#pragma unroll
+      for (int v = 0; v < 4; ++v) {
+        const auto r0 = __builtin_amdgcn_permlane16_swap(pp[0][v], pp[1][v], false, false);
+        pp[0][v] = r0[0];
+        pp[1][v] = r0[1];
+        const auto r1 = __builtin_amdgcn_permlane16_swap(pd[0][v], pd[1][v], false, false);
+        pd[0][v] = r1[0];
+        pd[1][v] = r1[1];
       }
       // dV^T += dO^T P and dK^T += Q^T dS over the tile's 32 query rows
 #pragma unroll
-      for (int dt = 0; dt < C::DT; ++dt)
+      for (int dt = 0; dt < DT16; ++dt) {
+        const s16x4 o_lo = lds_read_tr16(ot_lds + rtr[dt]);
+        const s16x4 o_hi = lds_read_tr16(ot_lds + rtr[dt] + 16 * C::ROWB);
+        const s16x4 q_lo = lds_read_tr16(qt_lds + rtr[dt]);
+        const s16x4 q_hi = lds_read_tr16(qt_lds + rtr[dt] + 16 * C::ROWB);
+        const s16x8 o8 = {o_lo[0], o_lo[1], o_lo[2], o_lo[3], o_hi[0], o_hi[1], o_hi[2], o_hi[3]};
+        const s16x8 q8 = {q_lo[0], q_lo[1], q_lo[2], q_lo[3], q_hi[0], q_hi[1], q_hi[2], q_hi[3]};
+        const bf16x8 ao = __builtin_bit_cast(bf16x8, o8), aq = __builtin_bit_cast(bf16x8, q8);
 #pragma unroll
-        for (int hh = 0; hh < 2; ++hh) {
-          const int rb = 16 * hh * C::ROWB;
-          const s16x4 o_lo = lds_read_tr16(ot_lds + rb + lo.tr[dt][0]);
-          const s16x4 o_hi = lds_read_tr16(ot_lds + rb + lo.tr[dt][1]);
-          const s16x4 q_lo = lds_read_tr16(qt_lds + rb + lo.tr[dt][0]);
-          const s16x4 q_hi = lds_read_tr16(qt_lds + rb + lo.tr[dt][1]);
-          const s16x8 o8 = {o_lo[0], o_lo[1], o_lo[2], o_lo[3], o_hi[0], o_hi[1], o_hi[2], o_hi[3]};
-          const s16x8 q8 = {q_lo[0], q_lo[1], q_lo[2], q_lo[3], q_hi[0], q_hi[1], q_hi[2], q_hi[3]};
-          dvt[dt] = mfma32(__builtin_bit_cast(bf16x8, o8), pb[hh], dvt[dt]);
-          dkt[dt] = mfma32(__builtin_bit_cast(bf16x8, q8), dsb[hh], dkt[dt]);
+        for (int kg = 0; kg < 2; ++kg) {
+          dv16[dt][kg] = mfma16(ao, __builtin_bit_cast(bf16x8, pp[kg]), dv16[dt][kg]);
+          dk16[dt][kg] = mfma16(aq, __builtin_bit_cast(bf16x8, pd[kg]), dk16[dt][kg]);
         }
+      }
     };
     auto iter = [&](int t, auto par) __attribute__((always_inline)) {
       constexpr int P = decltype(par)::value;
@@ -426,21 +489,24 @@ __global__ __launch_bounds__(64 * (BLOCK / 32), 256 / BLOCK) void bwd_dkdv_kerne
     if (t < T) iter(t, I0{});
   }
 
-  auto store_out = [&](__bf16* X, const f32x16 (&acc)[C::DT], float mul) __attribute__((always_inline)) {
-    if (key >= N) return;
-    const int64_t off = base_bh + (int64_t)key * tok_stride;
+  // lane stores columns 16 dt + 4 gq .. +3 of keys 32 kw + 16 kg + c16
+  auto store_out = [&](__bf16* X, const f32x4 (&acc)[DT16][2], float mul) __attribute__((always_inline)) {
 #pragma unroll
-    for (int dt = 0; dt < C::DT; ++dt)
+    for (int kg = 0; kg < 2; ++kg) {
+      const int ko = j * BLOCK + 32 * kw + 16 * kg + c16;
+      if (ko >= N) continue;
+      const int64_t off = base_bh + (int64_t)ko * tok_stride;
 #pragma unroll
-      for (int e4 = 0; e4 < 4; ++e4) {
+      for (int dt = 0; dt < DT16; ++dt) {
         bf16x4 v4;
 #pragma unroll
-        for (int e = 0; e < 4; ++e) v4[e] = (__bf16)(acc[dt][4 * e4 + e] * mul);
-        *reinterpret_cast<bf16x4*>(X + off + 32 * dt + 8 * e4 + 4 * g) = v4;
+        for (int e = 0; e < 4; ++e) v4[e] = (__bf16)(acc[dt][kg][e] * mul);
+        *reinterpret_cast<bf16x4*>(X + off + 16 * dt + 4 * gq) = v4;
       }
+    }
   };
-  store_out(dK, dkt, scale);
-  store_out(dV, dvt, 1.f);
+  store_out(dK, dk16, scale);
+  store_out(dV, dv16, 1.f);
 }
 
 template <int D, int BLOCK>
