@@ -96,6 +96,8 @@ def parse():
     # hold the step's only
     ap.add_argument("--no-varlen", action="store_true")
     ap.add_argument("--no-sweep", action="store_true")
+    # the backward's dQ from a recompute of S and dP instead of stored dS tiles
+    ap.add_argument("--recompute-dq", action="store_true")
     ap.add_argument("--sweep-steps", type=int, default=3)
     ap.add_argument("--cpu-seconds", type=float, default=15.0,
                     help="CPU time budget of the oracle baseline sample")
@@ -311,7 +313,10 @@ def time_varlen(ut, W, dev, stream, count: int = 8, reps: int = 10) -> dict:
         idx = ut.build_block_index(torch.from_numpy(bm).to(dev))
         o, lse = torch.empty_like(q), torch.empty((H, T), dtype=torch.float32, device=dev)
         dq, dk, dv = torch.empty_like(q), torch.empty_like(q), torch.empty_like(q)
-        ws = torch.empty(ut.ut_bsattn_bwd_varlen_workspace_size(T, H), dtype=torch.uint8, device=dev)
+        # room for every pair's dS tile; it also covers each sample's own call below
+        ws = torch.empty(ut.ut_bsattn_bwd_varlen_workspace_size_stored(len(lens), T, maxlen, H, blk,
+                                                                         idx["nnz"]),
+                         dtype=torch.uint8, device=dev)
 
         def packed():
             st = ut.ut_bsattn_fwd_varlen(q, k, v, o, lse, cu, maxlen, blk, idx["q_rowptr"],
@@ -355,13 +360,31 @@ def time_varlen(ut, W, dev, stream, count: int = 8, reps: int = 10) -> dict:
             "tflops_one_by_one": round(tot / (ms_loop * 1e-3) / 1e12, 2)}
 
 
+def bwd_workspace(ut, torch, n: int, H: int, blk: int, nnz: int, dev, stored: bool = True):
+    """The backward's workspace: with room for every pair's dS tile when that
+    takes at most half of the free device memory (dQ then comes from the
+    tiles), else the minimum (dQ recomputed). Returns (tensor, description)."""
+    base = ut.ut_bsattn_bwd_workspace_size(1, n, H)
+    full = ut.ut_bsattn_bwd_workspace_size_stored(1, n, H, blk, nnz)
+    free, _ = torch.cuda.mem_get_info(dev)
+    use = stored and full <= free // 2
+    size = full if use else base
+    info = {"dq_path": "stored dS tiles" if use else "recompute S and dP",
+            "workspace_bytes": size, "ds_tile_bytes": nnz * 2 * blk * blk if use else 0}
+    return torch.empty(size, dtype=torch.uint8, device=dev), info
+
+
 def kernel_rooflines(trace: list, steps: int, F: float, n: int, H: int, D: int,
-                     row_bytes: int, workload: str, rho: str) -> list:
+                     row_bytes: int, workload: str, rho: str, nnz: int, blk: int,
+                     dq_stored: bool) -> list:
     """Each attention and copy kernel of the timed steps against its own
     roofline. Algorithmic work per launch (F = forward FLOPs, 4 r c d per
-    retained pair): forward F; dK/dV its S, dP, dV and dK products, 2 F; dQ
-    its dQ product, F / 2 (it also recomputes S and dP, which are not
-    counted); the pre-pass reads O, dO and LSE and writes two fp32 planes;
+    retained pair): forward F; dK/dV its S, dP, dV and dK products, 2 F (the
+    variant that also stores the dS tiles is counted the same); dQ from the
+    stored tiles is bound by HBM: it reads every pair's 2 b^2-byte tile, K once
+    and writes dQ; dQ by recompute its dQ product, F / 2 (it also recomputes S
+    and dP, which are not counted), and nothing when the tiles serve every
+    query block; the pre-pass reads O, dO and LSE and writes two fp32 planes;
     gather and scatter read and write every kept row once."""
     out = []
     for r in trace:
@@ -370,7 +393,11 @@ def kernel_rooflines(trace: list, steps: int, F: float, n: int, H: int, D: int,
             bound, work = "mfma", F
         elif nm.startswith("bwd_dkdv"):
             bound, work = "mfma", 2 * F
+        elif nm.startswith("bwd_dq_stored"):
+            bound, work = "hbm", nnz * 2 * blk * blk + 2 * n * H * D * 2
         elif nm.startswith("bwd_dq"):
+            if dq_stored:
+                continue
             bound, work = "mfma", F / 2
         elif nm.startswith("bwd_prep"):
             bound, work = "hbm", n * H * (2 * D * 2 + 4 + 8)
@@ -422,7 +449,7 @@ def sweep(ut, W, dev, stream, base: dict, steps: int) -> list:
             o = torch.empty_like(q)
             lse = torch.empty((1, H, n), dtype=torch.float32, device=dev)
             dq, dk, dv = torch.empty_like(q), torch.empty_like(q), torch.empty_like(q)
-            ws = torch.empty(ut.ut_bsattn_bwd_workspace_size(1, n, H), dtype=torch.uint8, device=dev)
+            ws, ws_info = bwd_workspace(ut, torch, n, H, blk, idx["nnz"], dev, base["stored"])
 
             def fwd():
                 st = ut.ut_bsattn_fwd(q, k, v, o, lse, blk, idx["q_rowptr"], idx["q_cols"], sc)
@@ -449,8 +476,9 @@ def sweep(ut, W, dev, stream, base: dict, steps: int) -> list:
                     "ms_fwd_bwd": round(ms_f + ms_b, 4), "tflops_fwd_bwd": tf(3.5 * F, ms_f + ms_b),
                     "pct_peak_fwd_bwd": round(100 * 3.5 * F / ((ms_f + ms_b) * 1e-3) / 1e12
                                               / PEAK_BF16_TFLOPS, 2),
-                    "steps": steps})
+                    "bwd_dq_path": ws_info["dq_path"], "steps": steps})
         del inst, idx, o, lse, dq, dk, dv, ws
+        torch.cuda.empty_cache()   # the next configuration sizes its workspace by free memory
     return out
 
 
@@ -523,7 +551,7 @@ def power_sample(ut, dev, stream, q, k, v, do, idx, blk, sc, seconds: float = 6.
     o = torch.empty_like(q)
     lse = torch.empty((1, H, n), dtype=torch.float32, device=dev)
     dq, dk, dv = torch.empty_like(q), torch.empty_like(q), torch.empty_like(q)
-    ws = torch.empty(ut.ut_bsattn_bwd_workspace_size(1, n, H), dtype=torch.uint8, device=dev)
+    ws, ws_info = bwd_workspace(ut, torch, n, H, blk, idx["nnz"], dev)
     big = torch.empty(1 << 30, dtype=torch.uint8, device=dev)
     big2 = torch.empty_like(big)
     fwd = lambda: ut.ut_bsattn_fwd(q, k, v, o, lse, blk, idx["q_rowptr"], idx["q_cols"], sc)
@@ -614,7 +642,7 @@ def main():
     o = torch.empty_like(q)
     lse = torch.empty((1, H, n), dtype=torch.float32, device=dev)
     dq, dk, dv = torch.empty_like(q), torch.empty_like(q), torch.empty_like(q)
-    ws_bwd = torch.empty(ut.ut_bsattn_bwd_workspace_size(1, n, H), dtype=torch.uint8, device=dev)
+    ws_bwd, ws_info = bwd_workspace(ut, torch, n, H, blk, nnz, dev, not args.recompute_dq)
 
     stream = torch.cuda.current_stream()
     phases = ["drop", "index", "fwd", "bwd", "scatter"]
@@ -676,7 +704,7 @@ def main():
     attn_ms = per["fwd"] + per["bwd"]
     copy_bytes = 2 * n * wl.hidden * 2 + 4 * n if hidden is not None else 0
     kernels = kernel_rooflines(trace, args.steps, fwd_flops, n, H, D, wl.hidden * 2,
-                               wl.name, wl.rho)
+                               wl.name, wl.rho, nnz, blk, ws_info["ds_tile_bytes"] > 0)
     traced_total = sum(r["total_ms"] for r in trace)
     for e in kernels:
         e["share_of_step_kernels"] = round(e.pop("total_ms") / traced_total, 4)
@@ -702,6 +730,7 @@ def main():
                         f"forward + backward, gather and scatter of a {L} x {wl.hidden} bf16 state",
             "seq_len": L, "kept_tokens": n, "heads": H, "head_dim": D, "block": blk, "rho": wl.rho,
             "retained_pairs": nnz, "parallelism": "single GPU",
+            "bwd_dq_path": ws_info["dq_path"], "bwd_workspace_bytes": ws_info["workspace_bytes"],
         },
         "attention": {
             "ms_per_layer_fwd_bwd": round(attn_ms, 4),
@@ -731,7 +760,8 @@ def main():
     }
     if not args.no_sweep:
         result["sweep"] = sweep(ut, W, dev, stream, {"workload": wl.name, "q": q, "k": k, "v": v,
-                                                     "do": do}, args.sweep_steps)
+                                                     "do": do, "stored": not args.recompute_dq},
+                                args.sweep_steps)
     result["topk_mask"] = time_topk(ut, q, k, blk, W.kept_off_diagonal(wl.rho, nb), stream)
     result["fg_step"] = time_fg_step(ut, inst.fg_mask, wl.grid, dev, stream)
     result["decode_prep"] = time_decode_prep(ut, inst.fg_mask, wl.grid, dev, stream)

@@ -41,7 +41,7 @@
 extern "C" {
 #endif
 
-#define UT_ABI_VERSION 2
+#define UT_ABI_VERSION 3
 
 typedef enum {
   UT_OK = 0,
@@ -226,13 +226,30 @@ ut_status ut_bsattn_fwd(const void* q, const void* k, const void* v, void* o,
  * lse               fp32 [B, H, N].
  * dq, dk, dv        bf16 [B, N, H, D] outputs (fully overwritten).
  * q_rowptr, q_cols, kv_colptr, kv_rows  both lists of ut_build_block_index.
- * workspace         device scratch of ut_bsattn_bwd_workspace_size(B, N, H)
- *                   bytes (8 per query row), 16-byte aligned; holds the row
- *                   log-sum-exp in log2 units and -delta = -rowsum(dO o O)
- *                   as two planes of 4 bytes per row.
+ * workspace         device scratch, 16-byte aligned, of at least
+ *                   ut_bsattn_bwd_workspace_size(B, N, H) bytes (8 per query
+ *                   row): the row log-sum-exp in log2 units and
+ *                   -delta = -rowsum(dO o O) as two planes of 4 bytes per row.
+ *                   Bytes past that, from the next 256-byte boundary, hold
+ *                   a flag per query block (4 bytes each), a map of 4 bytes
+ *                   per pair and bf16 dS tiles of 2 block^2 bytes each (32
+ *                   KiB at block 128), one per retained pair in column-list
+ *                   order: the dK/dV pass writes the tiles that fit, and every
+ *                   query block whose tiles all fit takes dQ from them (one
+ *                   product per pair); the other query blocks recompute S and
+ *                   dP (three products per pair). The row and column lists
+ *                   must describe the same mask, as ut_build_block_index
+ *                   makes them. ut_bsattn_bwd_workspace_size_stored(B, N, H,
+ *                   block, nnz) is the size at which all nnz pairs fit.
+ *                   Either way the results agree to rounding (dS is bf16 in
+ *                   both).
  * Errors: as ut_bsattn_fwd, plus UT_ERR_WORKSPACE.
  * ---------------------------------------------------------------------- */
 size_t ut_bsattn_bwd_workspace_size(int32_t B, int32_t N, int32_t H);
+/* Workspace with room for the dS tiles of nnz retained pairs (the nnz of
+ * ut_build_block_index); 0 for block not 64 or 128, nnz < 0 or invalid sizes. */
+size_t ut_bsattn_bwd_workspace_size_stored(int32_t B, int32_t N, int32_t H,
+                                           int32_t block, int64_t nnz);
 ut_status ut_bsattn_bwd(const void* q, const void* k, const void* v,
                         const void* o, const void* dout, const float* lse,
                         void* dq, void* dk, void* dv, int32_t B, int32_t N,
@@ -288,7 +305,10 @@ ut_status ut_bsattn_bwd_noalloc(const void* q, const void* k, const void* v,
  *           over a [B, H, Nb, Nb] block mask. Sample b uses its leading
  *           ceil(len_b / block) block rows and columns; list entries past
  *           them are ignored, and its last block may be short.
- * workspace (backward) ut_bsattn_bwd_varlen_workspace_size(T, H) bytes.
+ * workspace (backward) at least ut_bsattn_bwd_varlen_workspace_size(T, H)
+ *           bytes; past the next 256-byte boundary, dS tiles as in
+ *           ut_bsattn_bwd (ut_bsattn_bwd_varlen_workspace_size_stored(B, T,
+ *           max_seqlen, H, block, nnz) holds all of them).
  * Offsets are clamped to [0, T] and lengths to max_seqlen inside the
  * kernels, so bad offsets cannot reach outside the tensors; tokens covered by
  * no sample are left unwritten. With UT_VALIDATE set, cu_seqlens is checked
@@ -302,6 +322,9 @@ ut_status ut_bsattn_fwd_varlen(const void* q, const void* k, const void* v,
                                const int32_t* q_rowptr, const int32_t* q_cols,
                                float softmax_scale, hipStream_t stream);
 size_t ut_bsattn_bwd_varlen_workspace_size(int64_t T, int32_t H);
+size_t ut_bsattn_bwd_varlen_workspace_size_stored(int32_t B, int64_t T,
+                                                  int32_t max_seqlen, int32_t H,
+                                                  int32_t block, int64_t nnz);
 ut_status ut_bsattn_bwd_varlen(const void* q, const void* k, const void* v,
                                const void* o, const void* dout,
                                const float* lse, void* dq, void* dk, void* dv,

@@ -33,8 +33,10 @@ EXPORTS = [
     "ut_last_error", "ut_abi_version", "ut_trace_enable", "ut_trace_read",
     "ut_drop_background_workspace_size", "ut_drop_background",
     "ut_scatter_foreground", "ut_build_block_index_workspace_size", "ut_build_block_index",
-    "ut_bsattn_fwd", "ut_bsattn_bwd_workspace_size", "ut_bsattn_bwd", "ut_bsattn_bwd_noalloc",
-    "ut_bsattn_fwd_varlen", "ut_bsattn_bwd_varlen_workspace_size", "ut_bsattn_bwd_varlen",
+    "ut_bsattn_fwd", "ut_bsattn_bwd_workspace_size", "ut_bsattn_bwd_workspace_size_stored",
+    "ut_bsattn_bwd", "ut_bsattn_bwd_noalloc",
+    "ut_bsattn_fwd_varlen", "ut_bsattn_bwd_varlen_workspace_size",
+    "ut_bsattn_bwd_varlen_workspace_size_stored", "ut_bsattn_bwd_varlen",
     "ut_topk_block_mask_workspace_size", "ut_topk_block_mask",
     "ut_euler_update_foreground", "ut_fg_flow_loss_workspace_size", "ut_fg_flow_loss",
     "ut_composite_latent", "ut_token_mask_workspace_size", "ut_token_mask_from_alpha",
@@ -68,6 +70,7 @@ _SIGS = {
                                         _vp]),
     "ut_bsattn_fwd": (_c.c_int, [_vp, _vp, _vp, _vp, _vp, _i32, _i32, _i32, _i32, _i32, _vp, _vp, _f32, _vp]),
     "ut_bsattn_bwd_workspace_size": (_sz, [_i32, _i32, _i32]),
+    "ut_bsattn_bwd_workspace_size_stored": (_sz, [_i32, _i32, _i32, _i32, _i64]),
     "ut_bsattn_bwd": (_c.c_int, [_vp, _vp, _vp, _vp, _vp, _vp, _vp, _vp, _vp, _i32, _i32, _i32, _i32, _i32,
                                  _vp, _vp, _vp, _vp, _f32, _vp, _sz, _vp]),
     "ut_bsattn_bwd_noalloc": (_c.c_int, [_vp, _vp, _vp, _vp, _vp, _vp, _vp, _vp, _vp, _i32, _i32, _i32, _i32,
@@ -75,6 +78,7 @@ _SIGS = {
     "ut_bsattn_fwd_varlen": (_c.c_int, [_vp, _vp, _vp, _vp, _vp, _vp, _i32, _i64, _i32, _i32, _i32, _i32,
                                         _vp, _vp, _f32, _vp]),
     "ut_bsattn_bwd_varlen_workspace_size": (_sz, [_i64, _i32]),
+    "ut_bsattn_bwd_varlen_workspace_size_stored": (_sz, [_i32, _i64, _i32, _i32, _i32, _i64]),
     "ut_bsattn_bwd_varlen": (_c.c_int, [_vp, _vp, _vp, _vp, _vp, _vp, _vp, _vp, _vp, _vp, _i32, _i64, _i32,
                                         _i32, _i32, _i32, _vp, _vp, _vp, _vp, _f32, _vp, _sz, _vp]),
     "ut_topk_block_mask_workspace_size": (_sz, [_i32, _i32, _i32, _i32, _i32]),
@@ -250,6 +254,13 @@ def ut_bsattn_bwd_workspace_size(B: int, N: int, H: int) -> int:
     return int(lib().ut_bsattn_bwd_workspace_size(B, N, H))
 
 
+def ut_bsattn_bwd_workspace_size_stored(B: int, N: int, H: int, block: int, nnz: int) -> int:
+    """Workspace bytes with room for the bf16 dS tiles of nnz retained pairs:
+    with it, dQ of every query block comes from the tiles the dK/dV pass
+    stores instead of a recompute of S and dP."""
+    return int(lib().ut_bsattn_bwd_workspace_size_stored(B, N, H, block, nnz))
+
+
 def ut_bsattn_bwd(q, k, v, o, dout, lse, dq, dk, dv, block: int, q_rowptr, q_cols, kv_colptr,
                   kv_rows, softmax_scale: float, workspace, stream=None) -> int:
     B, N, H, D, nb = _check_attn(q, k, v, block, q_rowptr, q_cols)
@@ -306,6 +317,11 @@ def ut_bsattn_fwd_varlen(q, k, v, o, lse, cu_seqlens, max_seqlen: int, block: in
 
 def ut_bsattn_bwd_varlen_workspace_size(T: int, H: int) -> int:
     return int(lib().ut_bsattn_bwd_varlen_workspace_size(T, H))
+
+
+def ut_bsattn_bwd_varlen_workspace_size_stored(B: int, T: int, max_seqlen: int, H: int, block: int,
+                                               nnz: int) -> int:
+    return int(lib().ut_bsattn_bwd_varlen_workspace_size_stored(B, T, max_seqlen, H, block, nnz))
 
 
 def ut_bsattn_bwd_varlen(q, k, v, o, dout, lse, dq, dk, dv, cu_seqlens, max_seqlen: int, block: int,
@@ -462,13 +478,29 @@ def bsattn_fwd(q, k, v, index, block: int, softmax_scale: float, stream=None):
     return o, lse
 
 
+def _ds_pairs(index, ds_pairs, block: int, base: int, device) -> int:
+    """dS tiles to make room for: all retained pairs by default, unless that
+    would take more than half of the device memory still free."""
+    if ds_pairs is None:
+        ds_pairs = int(index.get("nnz", 0))
+        free, _ = torch.cuda.mem_get_info(device)
+        if base + ds_pairs * 2 * block * block > free // 2:
+            ds_pairs = 0
+    return max(int(ds_pairs), 0)
+
+
 def bsattn_bwd(q, k, v, o, dout, lse, index, block: int, softmax_scale: float, workspace=None,
-               stream=None):
+               stream=None, ds_pairs=None):
+    """Gradients of bsattn_fwd. Without a workspace, one is allocated with
+    room for the dS tiles of `ds_pairs` pairs (default: every pair of the
+    index, if that fits in half the free device memory; 0: recompute dQ)."""
     B, N, H, D = q.shape
     dq, dk, dv = torch.empty_like(q), torch.empty_like(q), torch.empty_like(q)
     if workspace is None:
-        workspace = torch.empty(ut_bsattn_bwd_workspace_size(B, N, H), dtype=torch.uint8,
-                                device=q.device)
+        base = ut_bsattn_bwd_workspace_size(B, N, H)
+        n = _ds_pairs(index, ds_pairs, block, base, q.device)
+        size = ut_bsattn_bwd_workspace_size_stored(B, N, H, block, n) if n else base
+        workspace = torch.empty(size, dtype=torch.uint8, device=q.device)
     _raise("ut_bsattn_bwd", ut_bsattn_bwd(q, k, v, o, dout, lse, dq, dk, dv, block,
                                           index["q_rowptr"], index["q_cols"], index["kv_colptr"],
                                           index["kv_rows"], softmax_scale, workspace, stream))
@@ -489,12 +521,16 @@ def bsattn_fwd_varlen(q, k, v, cu_seqlens, max_seqlen: int, index, block: int, s
 
 
 def bsattn_bwd_varlen(q, k, v, o, dout, lse, cu_seqlens, max_seqlen: int, index, block: int,
-                      softmax_scale: float, workspace=None, stream=None):
+                      softmax_scale: float, workspace=None, stream=None, ds_pairs=None):
     T, H, D = q.shape
     dq, dk, dv = torch.zeros_like(q), torch.zeros_like(q), torch.zeros_like(q)
     if workspace is None:
-        workspace = torch.empty(max(ut_bsattn_bwd_varlen_workspace_size(T, H), 16), dtype=torch.uint8,
-                                device=q.device)
+        base = max(ut_bsattn_bwd_varlen_workspace_size(T, H), 16)
+        n = _ds_pairs(index, ds_pairs, block, base, q.device) if T > 0 else 0
+        B = cu_seqlens.numel() - 1
+        size = (ut_bsattn_bwd_varlen_workspace_size_stored(B, T, max_seqlen, H, block, n) if n
+                else base)
+        workspace = torch.empty(size, dtype=torch.uint8, device=q.device)
     _raise("ut_bsattn_bwd_varlen",
            ut_bsattn_bwd_varlen(q, k, v, o, dout, lse, dq, dk, dv, cu_seqlens, max_seqlen, block,
                                 index["q_rowptr"], index["q_cols"], index["kv_colptr"], index["kv_rows"],

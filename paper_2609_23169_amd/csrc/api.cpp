@@ -1,6 +1,7 @@
 // Host side of the C ABI declared in include/ultratex.h: argument validation,
 // workspace sizing, status codes and the per-thread error message. Every
 // check runs before any launch; no exception leaves this file.
+#include <algorithm>
 #include <cmath>
 #include <cstdarg>
 #include <cstdio>
@@ -110,6 +111,40 @@ ut_status check_ptr(const char* fn, const char* name, const void* p, uintptr_t a
     if (_s != UT_OK) return _s;       \
   } while (0)
 
+// ---- backward workspace: statistics planes, then the stored dS tiles ----
+// Layout past the statistics (each part 256-byte aligned): a flag per query
+// block row, the row-list entry -> tile map, then the tiles of 2 block^2 bytes.
+constexpr size_t kDsAlign = 256;
+size_t align_up(size_t x) { return (x + kDsAlign - 1) / kDsAlign * kDsAlign; }
+size_t tiles_bytes(int64_t m, int32_t block) {
+  return align_up((size_t)m * 4) + (size_t)m * 2 * block * block;
+}
+
+// Size with room for the dS tiles of nnz pairs (0 for invalid arguments).
+size_t stored_size(size_t stats_bytes, int64_t rows, int32_t block, int64_t nnz) {
+  if (stats_bytes == 0 || rows < 1 || (block != 64 && block != 128) || nnz < 0 ||
+      nnz > ((int64_t)1 << 31) - 1)
+    return 0;
+  return align_up(stats_bytes) + align_up((size_t)rows * 4) + tiles_bytes(nnz, block);
+}
+
+// The tiles a workspace of `bytes` holds past the statistics (none: recompute dQ).
+DsTiles ds_region(void* workspace, size_t bytes, size_t stats_bytes, int64_t rows, int32_t block) {
+  DsTiles r;
+  const size_t off = align_up(stats_bytes), flags = align_up((size_t)rows * 4);
+  if (!workspace || bytes <= off + flags) return r;
+  const size_t rem = bytes - off - flags;
+  int64_t m = std::min<int64_t>((int64_t)(rem / ((size_t)2 * block * block + 4)),
+                                ((int64_t)1 << 31) - 1);
+  while (m > 0 && tiles_bytes(m, block) > rem) --m;
+  if (m <= 0) return r;
+  char* base = static_cast<char*>(workspace) + off;
+  r.row_ok = reinterpret_cast<int32_t*>(base);
+  r.map = reinterpret_cast<int32_t*>(base + flags);
+  r.tiles = base + flags + align_up((size_t)m * 4);
+  r.max_pairs = m;
+  return r;
+}
 }  // namespace
 }  // namespace ut
 
@@ -298,6 +333,14 @@ size_t ut_bsattn_bwd_workspace_size(int32_t B, int32_t N, int32_t H) {
   return (size_t)B * H * N * 2 * sizeof(float);   // {LSE log2 e, delta} per query row
 }
 
+
+size_t ut_bsattn_bwd_workspace_size_stored(int32_t B, int32_t N, int32_t H, int32_t block,
+                                           int64_t nnz) {
+  if (block < 1) return 0;
+  return stored_size(ut_bsattn_bwd_workspace_size(B, N, H),
+                     (int64_t)B * H * (((int64_t)N + block - 1) / block), block, nnz);
+}
+
 ut_status ut_bsattn_bwd(const void* q, const void* k, const void* v, const void* o,
                         const void* dout, const float* lse, void* dq, void* dk, void* dv,
                         int32_t B, int32_t N, int32_t H, int32_t D, int32_t block,
@@ -326,8 +369,10 @@ ut_status ut_bsattn_bwd(const void* q, const void* k, const void* v, const void*
     UT_TRY(validate_lists(fn, "column lists", kv_colptr, kv_rows, (int64_t)B * H * sh.nblk,
                           sh.nblk, stream));
   }
+  const DsTiles ds = ds_region(workspace, workspace_bytes, need, (int64_t)B * H * sh.nblk, block);
   return check_hip(launch_bsattn_bwd(q, k, v, o, dout, lse, dq, dk, dv, sh, q_rowptr, q_cols,
-                                     kv_colptr, kv_rows, static_cast<float*>(workspace), stream),
+                                     kv_colptr, kv_rows, static_cast<float*>(workspace), ds,
+                                     stream),
                    "backward launch");
 }
 
@@ -358,7 +403,7 @@ ut_status ut_bsattn_bwd_noalloc(const void* q, const void* k, const void* v, con
   const AttnShape sh{B, N, H, D, block, (N + block - 1) / block, softmax_scale, nullptr,
                      (int64_t)B * N};
   return check_hip(launch_bsattn_bwd(q, k, v, o, dout, lse, dq, dk, dv, sh, q_rowptr, q_cols,
-                                     kv_colptr, kv_rows, ws, stream),
+                                     kv_colptr, kv_rows, ws, DsTiles{}, stream),
                    "backward launch");
 }
 
@@ -413,6 +458,13 @@ size_t ut_bsattn_bwd_varlen_workspace_size(int64_t T, int32_t H) {
   return (size_t)T * H * 2 * sizeof(float);
 }
 
+size_t ut_bsattn_bwd_varlen_workspace_size_stored(int32_t B, int64_t T, int32_t max_seqlen,
+                                                  int32_t H, int32_t block, int64_t nnz) {
+  if (B < 1 || max_seqlen < 1 || block < 1) return 0;
+  return stored_size(ut_bsattn_bwd_varlen_workspace_size(T, H),
+                     (int64_t)B * H * (((int64_t)max_seqlen + block - 1) / block), block, nnz);
+}
+
 ut_status ut_bsattn_bwd_varlen(const void* q, const void* k, const void* v, const void* o,
                                const void* dout, const float* lse, void* dq, void* dk, void* dv,
                                const int32_t* cu_seqlens, int32_t B, int64_t T,
@@ -446,8 +498,10 @@ ut_status ut_bsattn_bwd_varlen(const void* q, const void* k, const void* v, cons
     UT_TRY(validate_lists(fn, "column lists", kv_colptr, kv_rows, (int64_t)B * H * sh.nblk,
                           sh.nblk, stream));
   }
+  const DsTiles ds = ds_region(workspace, workspace_bytes, need, (int64_t)B * H * sh.nblk, block);
   return check_hip(launch_bsattn_bwd(q, k, v, o, dout, lse, dq, dk, dv, sh, q_rowptr, q_cols,
-                                     kv_colptr, kv_rows, static_cast<float*>(workspace), stream),
+                                     kv_colptr, kv_rows, static_cast<float*>(workspace), ds,
+                                     stream),
                    "backward launch");
 }
 

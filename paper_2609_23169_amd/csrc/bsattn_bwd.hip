@@ -23,8 +23,16 @@
 //           CU, so the two waves on each SIMD belong to different workgroups
 //           and never wait at the same barrier.
 //
-// The dQ pass recomputes S and dP instead of accumulating dQ with atomics
-// from the dK/dV pass. Tiles go from global memory straight into LDS with
+//   dQ from stored dS (when the workspace holds the tiles): the dK/dV pass
+//           also writes each retained pair's bf16 dS tile, at the pair's
+//           column-list position, and this pass takes dQ^T += K^T dS^T from
+//           it: one product per pair instead of three. A map pass, first,
+//           gives each row-list entry its tile and flags the query blocks whose
+//           tiles all fit in the workspace; the others keep the recompute pass
+//           above.
+//
+// Without stored tiles the dQ pass recomputes S and dP instead of accumulating
+// dQ with atomics from the dK/dV pass. Tiles go from global memory straight into LDS with
 // buffer loads; rows past N are outside the descriptor range and read as
 // zeros. For query rows past N that makes every contribution exactly zero
 // (zero Q and dO rows give dP = 0 and delta = 0, hence dS = 0 and P dO = 0).
@@ -39,6 +47,9 @@ namespace ut {
 namespace {
 
 constexpr float kLog2e = 1.4426950408889634f;
+// s_waitcnt immediate (gfx9 encoding: vmcnt bits 3:0 and 15:14, expcnt 6:4,
+// lgkmcnt 11:8): vmcnt(4) lgkmcnt(0), expcnt not waited for.
+constexpr int kWaitVm4Lgkm0 = 0x0074;
 
 // ---------------------------------------------------------------------------
 // prep: two planes over the statistics rows, in the layout of LSE ([B, H, N]
@@ -118,6 +129,42 @@ struct LaneOffsets {
 };
 
 // ---------------------------------------------------------------------------
+// map: for row-list entry p (pair (i, j) of query block row r) the column-list
+// position e of the same pair, which indexes its dS tile, by a binary search
+// of column j's ascending list for i; and row_ok[r] = 1 when every tile of the
+// row lies below max_pairs (its dQ then comes from the tiles). One wave per
+// query block row; entries at or past max_pairs get no map entry.
+// ---------------------------------------------------------------------------
+__global__ __launch_bounds__(64) void bwd_ds_map_kernel(
+    const int32_t* __restrict__ rowptr, const int32_t* __restrict__ cols,
+    const int32_t* __restrict__ colptr, const int32_t* __restrict__ rows_list, int nblk,
+    int64_t max_pairs, int32_t* __restrict__ map, int32_t* __restrict__ row_ok) {
+  const int64_t r = blockIdx.x;
+  const int i = (int)(r % nblk);
+  const int64_t cbase = r - i;   // (b, h) * nblk
+  const int p0 = rowptr[r], p1 = rowptr[r + 1];
+  bool ok = (int64_t)p1 <= max_pairs;
+  for (int p = p0 + (int)threadIdx.x; p < p1 && (int64_t)p < max_pairs; p += 64) {
+    const int j = cols[p];
+    int e = -1;
+    if (j >= 0 && j < nblk) {
+      const int lo0 = colptr[cbase + j], hi0 = colptr[cbase + j + 1];
+      int lo = lo0, hi = hi0;
+      while (lo < hi) {
+        const int mid = (lo + hi) >> 1;
+        if (rows_list[mid] < i) lo = mid + 1;
+        else hi = mid;
+      }
+      if (lo < hi0 && rows_list[lo] == i) e = lo;
+    }
+    map[p] = e;
+    ok = ok && e >= 0 && (int64_t)e < max_pairs;
+  }
+  ok = __all(ok);
+  if (threadIdx.x == 0) row_ok[r] = ok ? 1 : 0;
+}
+
+// ---------------------------------------------------------------------------
 // dQ: query-stationary over the row lists
 // ---------------------------------------------------------------------------
 template <int D, int BLOCK>
@@ -125,7 +172,8 @@ __global__ __launch_bounds__(64 * (BLOCK / 32), (BLOCK == 128 || D == 64) ? 2 : 
     const __bf16* __restrict__ Q, const __bf16* __restrict__ K, const __bf16* __restrict__ V,
     const __bf16* __restrict__ dO, const float* __restrict__ aux, __bf16* __restrict__ dQ, int B,
     int N_all, int H, int nblk, float scale, const int32_t* __restrict__ rowptr,
-    const int32_t* __restrict__ cols, const int32_t* __restrict__ cu_seqlens, int64_t T_tok) {
+    const int32_t* __restrict__ cols, const int32_t* __restrict__ cu_seqlens, int64_t T_tok,
+    const int32_t* __restrict__ row_ok) {
   using C = BwdCfg<D, BLOCK, BLOCK / 32>;
   __shared__ __attribute__((aligned(1024))) char k_lds0[C::TILEB];
   __shared__ __attribute__((aligned(1024))) char k_lds1[C::TILEB];
@@ -136,6 +184,7 @@ __global__ __launch_bounds__(64 * (BLOCK / 32), (BLOCK == 128 || D == 64) ? 2 : 
   const int w = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int l32 = lane & 31, g = lane >> 5;
   const int64_t lt = blockIdx.x;   // tile order: see the launcher
+  if (row_ok && row_ok[lt]) return;   // dQ comes from the stored dS tiles
   const int i = (int)(lt % nblk);
   const int64_t bh = lt / nblk;
   const int h = (int)(bh % H), b = (int)(bh / H);
@@ -304,15 +353,206 @@ __global__ __launch_bounds__(64 * (BLOCK / 32), (BLOCK == 128 || D == 64) ? 2 : 
 }
 
 // ---------------------------------------------------------------------------
-// dK, dV: key-stationary over the column lists, one wave per 32 keys
+// dQ from the stored dS tiles: query-stationary over the row lists like the
+// recompute pass, one product per pair. Wave w owns queries 32 w .. 32 w + 31
+// of block i; per 64-key tile it takes the tile's K rows (shared, in LDS) and
+// its own two 2 KB dS chunks (32 queries x 32 keys each, streamed into LDS by
+// each wave for itself), and accumulates dQ^T += K^T dS^T on 16x16x32 with
+// both operands from transposing LDS reads. Query blocks without row_ok are
+// left to the recompute pass; for the others map[p] < max_pairs is the tile of
+// every entry p.
 // ---------------------------------------------------------------------------
 template <int D, int BLOCK>
+__global__ __launch_bounds__(64 * (BLOCK / 32), 2) void bwd_dq_stored_kernel(
+    const __bf16* __restrict__ K, const char* __restrict__ ds, __bf16* __restrict__ dQ,
+    int N_all, int H, int nblk, float scale, const int32_t* __restrict__ rowptr,
+    const int32_t* __restrict__ cols, const int32_t* __restrict__ cu_seqlens, int64_t T_tok,
+    const int32_t* __restrict__ map, const int32_t* __restrict__ row_ok) {
+  constexpr int NW = BLOCK / 32;
+  using C = BwdCfg<D, BLOCK, NW>;
+  constexpr int PAIRB = 2 * BLOCK * BLOCK;   // one pair's dS tile
+  constexpr int WSB = 2 * 2048;              // one wave's dS chunks of one 64-key tile
+  // K tiles one tile ahead (two buffers), dS chunks two tiles ahead (three):
+  // the dS stream comes from HBM and needs more bytes in flight
+  __shared__ __attribute__((aligned(1024))) char k_lds0[C::TILEB];
+  __shared__ __attribute__((aligned(1024))) char k_lds1[C::TILEB];
+  __shared__ __attribute__((aligned(1024))) char s_lds0[NW * WSB];
+  __shared__ __attribute__((aligned(1024))) char s_lds1[NW * WSB];
+  __shared__ __attribute__((aligned(1024))) char s_lds2[NW * WSB];
+
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int w = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int64_t lt = blockIdx.x;
+  if (!row_ok[lt]) return;   // not all stored: the recompute pass takes it
+  const int p0 = rowptr[lt], pe = rowptr[lt + 1];
+  const int i = (int)(lt % nblk);
+  const int64_t bh = lt / nblk;
+  const int h = (int)(bh % H), b = (int)(bh / H);
+  const int64_t tok_stride = (int64_t)H * D;
+  const SampleRows sr = sample_rows(cu_seqlens, T_tok, b, h, H, N_all);
+  const int N = sr.n;
+  if (N <= 0 || i * BLOCK >= N) return;
+  const int64_t base_bh = sr.tok0 * tok_stride + (int64_t)h * D;
+  int p1 = pe;
+  while (p1 > p0 && cols[p1 - 1] >= (N + BLOCK - 1) / BLOCK) --p1;   // past the sample
+  const int T = (p1 - p0) * C::SUBS;
+
+  constexpr int DT16 = D / 16;
+  const int c16 = lane & 15, gq = lane >> 4;
+  f32x4 dq16[DT16][2];
+#pragma unroll
+  for (int dt = 0; dt < DT16; ++dt) dq16[dt][0] = dq16[dt][1] = f32x4{};
+
+  if (T > 0) {
+    const LaneOffsets<C> lo(w, lane, tok_stride);
+    // K^T operand for d tile dt: key rows base(gq) + (c16 >> 2) (slots 0..3)
+    // and the same + 16 (slots 4..7), base(gq) = 8 (gq & 1) + 4 (gq >> 1).
+    int ktr[DT16];
+#pragma unroll
+    for (int dt = 0; dt < DT16; ++dt) {
+      const int d = 16 * dt + 4 * (c16 & 3);
+      ktr[dt] = lds_off<C::CPR>(8 * (gq & 1) + 4 * (gq >> 1) + (c16 >> 2), d >> 3) + 2 * (d & 7);
+    }
+    // dS^T operand with the same key slots: lane c16 of group gq reads key
+    // base(gq) + (c16 >> 2) (+16 for slots 4..7) at queries 16 qg + 4 u .. +3,
+    // u = c16 & 3, which the storing lane (gs, cs) holds: base(gs) = 4 u,
+    // cs = the key within its 16.
+    const int u = c16 & 3;
+    const int gs = ((u & 1) << 1) | (u >> 1);
+    const int cs = 8 * (gq & 1) + 4 * (gq >> 1) + (c16 >> 2);
+    const int sb = w * WSB + 16 * (16 * gs + (cs ^ (4 * (gs & 1))));
+
+    auto load_k = [&](int t, char* kdst) __attribute__((always_inline)) {
+      const int p = p0 + t / C::SUBS, hh = t % C::SUBS;
+      const int key0 = cols[p] * BLOCK + hh * C::ST;
+      const int nrec = key0 < N ? (N - key0 - 1) * (int)(tok_stride * 2) + 2 * D : 0;
+      const __amdgpu_buffer_rsrc_t rk = buffer_rsrc(K + base_bh + (int64_t)key0 * tok_stride, nrec);
+#pragma unroll
+      for (int v = 0; v < C::IPW; ++v) buffer_load_lds16(rk, kdst + (w * C::IPW + v) * 1024, lo.dma[v]);
+    };
+    // this wave's dS chunks of tile t: kSLoads direct loads, issued last
+    constexpr int kSLoads = WSB / 1024;
+    auto load_s = [&](int t, char* sdst) __attribute__((always_inline)) {
+      const int p = p0 + t / C::SUBS, hh = t % C::SUBS;
+      const __amdgpu_buffer_rsrc_t rs =
+          buffer_rsrc(ds + (int64_t)map[p] * PAIRB + (w * NW + 2 * hh) * 2048, WSB);
+#pragma unroll
+      for (int v = 0; v < kSLoads; ++v)
+        buffer_load_lds16(rs, sdst + w * WSB + v * 1024, v * 1024 + 16 * lane);
+    };
+
+    auto step = [&](const char* kt_lds, const char* st_lds) __attribute__((always_inline)) {
+#pragma unroll
+      for (int kt = 0; kt < 2; ++kt) {   // 32-key halves: one dS chunk each
+        bf16x8 bq[2];
+#pragma unroll
+        for (int qg = 0; qg < 2; ++qg) {
+          const char* sp = st_lds + sb + kt * 2048 + qg * 1024;
+          const s16x4 l4 = lds_read_tr16(sp);
+          const s16x4 h4 = lds_read_tr16(sp + 8);
+          const s16x8 s8 = {l4[0], l4[1], l4[2], l4[3], h4[0], h4[1], h4[2], h4[3]};
+          bq[qg] = __builtin_bit_cast(bf16x8, s8);
+        }
+#pragma unroll
+        for (int dt = 0; dt < DT16; ++dt) {
+          const char* kb = kt_lds + 32 * kt * C::ROWB + ktr[dt];
+          const s16x4 l4 = lds_read_tr16(kb);
+          const s16x4 h4 = lds_read_tr16(kb + 16 * C::ROWB);
+          const s16x8 k8 = {l4[0], l4[1], l4[2], l4[3], h4[0], h4[1], h4[2], h4[3]};
+          const bf16x8 av = __builtin_bit_cast(bf16x8, k8);
+          dq16[dt][0] = mfma16(av, bq[0], dq16[dt][0]);
+          dq16[dt][1] = mfma16(av, bq[1], dq16[dt][1]);
+        }
+      }
+    };
+    auto sbuf = [&](auto slot) __attribute__((always_inline)) -> char* {
+      constexpr int S = decltype(slot)::value;
+      return S == 0 ? s_lds0 : S == 1 ? s_lds1 : s_lds2;
+    };
+    // Tile t uses K buffer t % 2 and dS buffer t % 3 (KP, SP).
+    auto iter = [&](int t, auto kpar, auto sslot) __attribute__((always_inline)) {
+      constexpr int KP = decltype(kpar)::value, SP = decltype(sslot)::value;
+      if (t + 1 < T) load_k(t + 1, KP ? k_lds0 : k_lds1);
+      const bool ahead = t + 2 < T;
+      if (ahead) load_s(t + 2, sbuf(std::integral_constant<int, (SP + 2) % 3>{}));
+      // keep the loads ahead of this tile's work (the scheduler would sink them
+      // to the wait at its end, exposing their latency)
+      __builtin_amdgcn_sched_barrier(0);
+      step(KP ? k_lds1 : k_lds0, sbuf(sslot));
+      if (ahead) {
+        // Vector memory operations complete in issue order, so vmcnt(kSLoads)
+        // means every load but tile t + 2's dS has landed. The fences order
+        // LDS only: a full workgroup fence would wait for those loads too.
+        __builtin_amdgcn_s_waitcnt(kWaitVm4Lgkm0);
+        __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup", "local");
+        __builtin_amdgcn_s_barrier();
+        __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup", "local");
+      } else {
+        __builtin_amdgcn_s_waitcnt(0);
+        __syncthreads();
+      }
+    };
+    static_assert(kSLoads == 4, "the wait below counts four dS loads");
+
+    load_k(0, k_lds0);
+    load_s(0, s_lds0);
+    if (T > 1) load_s(1, s_lds1);
+    __builtin_amdgcn_s_waitcnt(0);
+    __syncthreads();
+    using I0 = std::integral_constant<int, 0>;
+    using I1 = std::integral_constant<int, 1>;
+    using I2 = std::integral_constant<int, 2>;
+    int t = 0;
+    for (; t + 5 < T; t += 6) {
+      iter(t, I0{}, I0{});
+      iter(t + 1, I1{}, I1{});
+      iter(t + 2, I0{}, I2{});
+      iter(t + 3, I1{}, I0{});
+      iter(t + 4, I0{}, I1{});
+      iter(t + 5, I1{}, I2{});
+    }
+    if (t < T) iter(t, I0{}, I0{});
+    if (t + 1 < T) iter(t + 1, I1{}, I1{});
+    if (t + 2 < T) iter(t + 2, I0{}, I2{});
+    if (t + 3 < T) iter(t + 3, I1{}, I0{});
+    if (t + 4 < T) iter(t + 4, I0{}, I1{});
+  }
+
+#pragma unroll
+  for (int qg = 0; qg < 2; ++qg) {
+    const int qo = i * BLOCK + 32 * w + 16 * qg + c16;
+    if (qo >= N) continue;
+    const int64_t off = base_bh + (int64_t)qo * tok_stride;
+#pragma unroll
+    for (int dt = 0; dt < DT16; ++dt) {
+      bf16x4 v4;
+#pragma unroll
+      for (int e = 0; e < 4; ++e) v4[e] = (__bf16)(dq16[dt][qg][e] * scale);
+      *reinterpret_cast<bf16x4*>(dQ + off + 16 * dt + 4 * gq) = v4;
+    }
+  }
+}
+
+// ---------------------------------------------------------------------------
+// dK, dV: key-stationary over the column lists, one wave per 32 keys
+// ---------------------------------------------------------------------------
+// With STORE, the pass also writes each pair's dS as bf16 into `ds` at the
+// pair's column-list position e (tiles of pairs e >= max_pairs are not written):
+// 2 BLOCK^2 bytes per pair, as (BLOCK/32)^2 chunks of 2 KB, chunk
+// (query tile, key group) holding dS for 32 queries x 32 keys. Within a
+// chunk, the lane (gq, c16) that holds keys c16 and 16 + c16 after the
+// exchange stores, at 16-byte unit 16 gq + (c16 ^ 4 (gq & 1)) of half x, its
+// four queries base(gq) + 16 x + (0..3) for key c16 and then for key
+// 16 + c16. Each store instruction writes 1 KB contiguously; the dQ pass
+// reads the chunk back with transposing LDS reads.
+template <int D, int BLOCK, bool STORE>
 __global__ __launch_bounds__(64 * (BLOCK / 32), 256 / BLOCK) void bwd_dkdv_kernel(
     const __bf16* __restrict__ Q, const __bf16* __restrict__ K, const __bf16* __restrict__ V,
     const __bf16* __restrict__ dO, const float* __restrict__ aux, __bf16* __restrict__ dK,
     __bf16* __restrict__ dV, int B, int N_all, int H, int nblk, float scale,
     const int32_t* __restrict__ colptr, const int32_t* __restrict__ rows_list,
-    const int32_t* __restrict__ cu_seqlens, int64_t T_tok) {
+    const int32_t* __restrict__ cu_seqlens, int64_t T_tok, char* __restrict__ ds,
+    int64_t max_pairs) {
   constexpr int NK = BLOCK / 32;        // key groups (one wave each)
   using C = BwdCfg<D, BLOCK, NK, 32>;
   constexpr int AUXB = 2048;            // 32 rows of each plane, one 1 KB load each
@@ -405,7 +645,25 @@ __global__ __launch_bounds__(64 * (BLOCK / 32), 256 / BLOCK) void bwd_dkdv_kerne
     };
     const float c2 = scale * kLog2e;
 
-    auto step = [&](const char* qt_lds, const char* ot_lds, const char* at_lds)
+    // dS of the last computed tile, not yet stored (pos -1: nothing to store)
+    struct {
+      u32x4 u0, u1;
+      int pos = -1, sub = 0;
+    } pend;
+    auto store_pending = [&]() __attribute__((always_inline)) {
+      if (pend.pos < 0) return;
+      u32x4 u0 = pend.u0, u1 = pend.u1;
+      if ((j + 1) * BLOCK > N) {   // keys past N store zeros (their P is not 0)
+        const int k0 = j * BLOCK + 32 * kw + c16;
+        if (k0 >= N) u0[0] = u0[1] = u1[0] = u1[1] = 0u;
+        if (k0 + 16 >= N) u0[2] = u0[3] = u1[2] = u1[3] = 0u;
+      }
+      char* dst = ds + (int64_t)pend.pos * (2 * BLOCK * BLOCK) + (pend.sub * NK + kw) * 2048 +
+                  16 * (16 * gq + (c16 ^ (4 * (gq & 1))));
+      __builtin_nontemporal_store(u0, reinterpret_cast<u32x4*>(dst));
+      __builtin_nontemporal_store(u1, reinterpret_cast<u32x4*>(dst + 1024));
+    };
+    auto step = [&](int t, int pos, const char* qt_lds, const char* ot_lds, const char* at_lds)
         __attribute__((always_inline)) {
       // S = Q K^T and dP = dO V^T for the tile's 32 query rows
       const float* const a_pl = reinterpret_cast<const float*>(at_lds) + 4 * g;
@@ -451,6 +709,13 @@ __global__ __launch_bounds__(64 * (BLOCK / 32), 256 / BLOCK) void bwd_dkdv_kerne
         pd[0][v] = r1[0];
         pd[1][v] = r1[1];
       }
+      if constexpr (STORE) {
+        // this tile's dS, stored by the next iteration (or after the loop)
+        pend.u0 = u32x4{pd[0][0], pd[0][1], pd[1][0], pd[1][1]};   // queries base(gq) + 0..3
+        pend.u1 = u32x4{pd[0][2], pd[0][3], pd[1][2], pd[1][3]};   // queries base(gq) + 16..19
+        pend.pos = pos;
+        pend.sub = t % C::SUBS;
+      }
       // dV^T += dO^T P and dK^T += Q^T dS over the tile's 32 query rows
 #pragma unroll
       for (int dt = 0; dt < DT16; ++dt) {
@@ -470,8 +735,17 @@ __global__ __launch_bounds__(64 * (BLOCK / 32), 256 / BLOCK) void bwd_dkdv_kerne
     };
     auto iter = [&](int t, auto par) __attribute__((always_inline)) {
       constexpr int P = decltype(par)::value;
+      // column-list position of this tile's pair, or -1 (no dS store)
+      int pos = -1;
+      if constexpr (STORE) {
+        const int e = p0 + t / C::SUBS;
+        pos = (int64_t)e < max_pairs ? e : -1;
+        // the previous tile's dS: a whole iteration to reach L2 before the
+        // wait at this iteration's end
+        store_pending();
+      }
       if (t + 1 < T) load_tile(t + 1, P ? q_lds0 : q_lds1, P ? o_lds0 : o_lds1, P ? a_lds0 : a_lds1);
-      step(P ? q_lds1 : q_lds0, P ? o_lds1 : o_lds0, P ? a_lds1 : a_lds0);
+      step(t, pos, P ? q_lds1 : q_lds0, P ? o_lds1 : o_lds0, P ? a_lds1 : a_lds0);
       __builtin_amdgcn_s_waitcnt(0);
       __syncthreads();
     };
@@ -487,6 +761,7 @@ __global__ __launch_bounds__(64 * (BLOCK / 32), 256 / BLOCK) void bwd_dkdv_kerne
       iter(t + 1, I1{});
     }
     if (t < T) iter(t, I0{});
+    if constexpr (STORE) store_pending();
   }
 
   // lane stores columns 16 dt + 4 gq .. +3 of keys 32 kw + 16 kg + c16
@@ -513,32 +788,53 @@ template <int D, int BLOCK>
 hipError_t launch_bwd_t(const void* q, const void* k, const void* v, const void* o,
                         const void* dout, const float* lse, void* dq, void* dk, void* dv,
                         const AttnShape& sh, const int32_t* rowptr, const int32_t* cols,
-                        const int32_t* colptr, const int32_t* rows, float* ws, hipStream_t s) {
+                        const int32_t* colptr, const int32_t* rows, float* aux, const DsTiles& ds,
+                        hipStream_t s) {
   auto bf = [](const void* p) { return static_cast<const __bf16*>(p); };
-  float* aux = ws;
   const int64_t rows_total = sh.T * sh.H * (D / 8);
+  // One workgroup per (b, h, block) in plain order. Workgroups go round-robin
+  // to the 8 XCDs, so all XCDs work on the same few heads at once (their K and
+  // V stay in the shared last-level cache) and a run of heavy blocks is spread
+  // over every XCD.
+  const int64_t nrow = (int64_t)sh.B * sh.H * sh.nblk;
+  const dim3 grid((unsigned)nrow);
+  const bool store = ds.max_pairs > 0 && ds.tiles && ds.map && ds.row_ok;
+  if (store) {
+    TraceScope ts_(s, "bwd_ds_map");
+    hipLaunchKernelGGL(bwd_ds_map_kernel, grid, dim3(64), 0, s, rowptr, cols, colptr, rows, sh.nblk,
+                       ds.max_pairs, ds.map, ds.row_ok);
+  }
   {
     TraceScope ts_(s, "bwd_prep", D);
     hipLaunchKernelGGL((bwd_prep_kernel<D>), dim3((unsigned)((rows_total + 255) / 256)), dim3(256), 0,
                      s, bf(o), bf(dout), lse, aux, sh.T, sh.N, sh.H, sh.cu != nullptr);
   }
-  // One workgroup per (b, h, block) in plain order. Workgroups go round-robin
-  // to the 8 XCDs, so all XCDs work on the same few heads at once (their K and
-  // V stay in the shared last-level cache) and a run of heavy blocks is spread
-  // over every XCD.
-  const dim3 grid((unsigned)((int64_t)sh.B * sh.H * sh.nblk));
-  {
-    TraceScope ts_(s, "bwd_dkdv", D, BLOCK);
-    hipLaunchKernelGGL((bwd_dkdv_kernel<D, BLOCK>), grid, dim3(64 * (BLOCK / 32)), 0, s,
+  if (store) {
+    TraceScope ts_(s, "bwd_dkdv_store", D, BLOCK);
+    hipLaunchKernelGGL((bwd_dkdv_kernel<D, BLOCK, true>), grid, dim3(64 * (BLOCK / 32)), 0, s,
                      bf(q), bf(k), bf(v), bf(dout), aux, static_cast<__bf16*>(dk),
                      static_cast<__bf16*>(dv), sh.B, sh.N, sh.H, sh.nblk, sh.scale, colptr, rows,
-                     sh.cu, sh.T);
+                     sh.cu, sh.T, ds.tiles, ds.max_pairs);
+  } else {
+    TraceScope ts_(s, "bwd_dkdv", D, BLOCK);
+    hipLaunchKernelGGL((bwd_dkdv_kernel<D, BLOCK, false>), grid, dim3(64 * (BLOCK / 32)), 0, s,
+                     bf(q), bf(k), bf(v), bf(dout), aux, static_cast<__bf16*>(dk),
+                     static_cast<__bf16*>(dv), sh.B, sh.N, sh.H, sh.nblk, sh.scale, colptr, rows,
+                     sh.cu, sh.T, static_cast<char*>(nullptr), (int64_t)0);
+  }
+  if (store) {
+    TraceScope ts_(s, "bwd_dq_stored", D, BLOCK);
+    hipLaunchKernelGGL((bwd_dq_stored_kernel<D, BLOCK>), grid, dim3(64 * (BLOCK / 32)), 0, s,
+                     bf(k), static_cast<const char*>(ds.tiles), static_cast<__bf16*>(dq), sh.N, sh.H,
+                     sh.nblk, sh.scale, rowptr, cols, sh.cu, sh.T, ds.map, ds.row_ok);
   }
   {
+    // every query block without row_ok (all of them without stored tiles)
     TraceScope ts_(s, "bwd_dq", D, BLOCK);
     hipLaunchKernelGGL((bwd_dq_kernel<D, BLOCK>), grid, dim3(64 * (BLOCK / 32)), 0, s,
                      bf(q), bf(k), bf(v), bf(dout), aux, static_cast<__bf16*>(dq), sh.B, sh.N, sh.H,
-                     sh.nblk, sh.scale, rowptr, cols, sh.cu, sh.T);
+                     sh.nblk, sh.scale, rowptr, cols, sh.cu, sh.T,
+                     store ? static_cast<const int32_t*>(ds.row_ok) : nullptr);
   }
   return hipGetLastError();
 }
@@ -581,12 +877,12 @@ hipError_t noalloc_scratch(hipStream_t s, float** ptr) {
 hipError_t launch_bsattn_bwd(const void* q, const void* k, const void* v, const void* o,
                              const void* dout, const float* lse, void* dq, void* dk, void* dv,
                              const AttnShape& sh, const int32_t* rowptr, const int32_t* cols,
-                             const int32_t* colptr, const int32_t* rows, float* delta,
-                             hipStream_t s) {
+                             const int32_t* colptr, const int32_t* rows, float* aux,
+                             const DsTiles& ds, hipStream_t s) {
 #define UT_BWD(DD, BB)                                                                        \
   if (sh.D == DD && sh.block == BB)                                                           \
     return launch_bwd_t<DD, BB>(q, k, v, o, dout, lse, dq, dk, dv, sh, rowptr, cols, colptr, \
-                                rows, delta, s);
+                                rows, aux, ds, s);
   UT_BWD(128, 128)
   UT_BWD(128, 64)
   UT_BWD(64, 128)

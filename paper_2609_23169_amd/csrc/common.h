@@ -66,11 +66,20 @@ struct AttnShape {
 hipError_t launch_bsattn_fwd(const void* q, const void* k, const void* v, void* o, float* lse,
                              const AttnShape& sh, const int32_t* rowptr, const int32_t* cols,
                              hipStream_t s);
+// Where the backward keeps stored dS tiles (max_pairs = 0: none; dQ is then
+// recomputed for every query block).
+struct DsTiles {
+  int32_t* row_ok = nullptr;   // [B H Nq] query block takes dQ from the tiles
+  int32_t* map = nullptr;      // [max_pairs] row-list entry -> tile (column-list position)
+  char* tiles = nullptr;       // [max_pairs][2 block^2] bf16 dS
+  int64_t max_pairs = 0;
+};
+// Backward. `aux` holds the two statistics planes (8 bytes per query row).
 hipError_t launch_bsattn_bwd(const void* q, const void* k, const void* v, const void* o,
                              const void* dout, const float* lse, void* dq, void* dk, void* dv,
                              const AttnShape& sh, const int32_t* rowptr, const int32_t* cols,
-                             const int32_t* colptr, const int32_t* rows, float* delta,
-                             hipStream_t s);
+                             const int32_t* colptr, const int32_t* rows, float* aux,
+                             const DsTiles& ds, hipStream_t s);
 
 // Scratch of ut_bsattn_bwd_noalloc: a file-scope device array in
 // bsattn_bwd.hip, one copy per GPU, holding the backward's two statistics

@@ -28,7 +28,7 @@ def test_library_exports_every_declared_symbol():
     lib = ut.lib()
     for name in declared_functions():
         assert hasattr(lib, name), name
-    assert lib.ut_abi_version() == 2
+    assert lib.ut_abi_version() == 3
 
 
 def test_trace_switch_and_empty_read():
@@ -60,6 +60,30 @@ def test_workspace_sizes():
     assert ut.ut_bsattn_bwd_workspace_size(1, 77586, 24) == 77586 * 24 * 8
     assert ut.ut_bsattn_bwd_varlen_workspace_size(77586, 24) == 77586 * 24 * 8
     assert ut.ut_bsattn_bwd_varlen_workspace_size(0, 24) == 0
+
+
+def test_stored_ds_workspace_sizes():
+    # statistics planes, a flag per query block row, the entry -> tile map and
+    # the tiles of 2 block^2 bytes, each part padded to 256 bytes
+    pad = lambda x: -(-x // 256) * 256
+    rows = 1 * 3 * 8                      # B H ceil(1000 / 128)
+    head = pad(1000 * 3 * 8) + pad(rows * 4)
+    assert ut.ut_bsattn_bwd_workspace_size_stored(1, 1000, 3, 128, 0) == head
+    assert ut.ut_bsattn_bwd_workspace_size_stored(1, 1000, 3, 128, 10) == head + pad(40) + 10 * 32768
+    rows64 = 1 * 3 * 16
+    assert (ut.ut_bsattn_bwd_workspace_size_stored(1, 1000, 3, 64, 10)
+            == pad(1000 * 3 * 8) + pad(rows64 * 4) + pad(40) + 10 * 8192)
+    # the 2K training workload at rho = 0.1: 882,792 pairs of 32 KiB
+    big = ut.ut_bsattn_bwd_workspace_size_stored(1, 77060, 24, 128, 882792)
+    assert big == pad(77060 * 24 * 8) + pad(24 * 603 * 4) + pad(882792 * 4) + 882792 * 32768
+    for args in [(1, 1000, 3, 96, 10), (1, 1000, 3, 128, -1), (0, 1000, 3, 128, 10),
+                 (1, 0, 3, 128, 10), (1, 1000, 3, 0, 10)]:
+        assert ut.ut_bsattn_bwd_workspace_size_stored(*args) == 0, args
+    # packed samples: B = 2, max_seqlen 700 -> 6 blocks per sample
+    assert (ut.ut_bsattn_bwd_varlen_workspace_size_stored(2, 1000, 700, 3, 128, 10)
+            == pad(1000 * 3 * 8) + pad(2 * 3 * 6 * 4) + pad(40) + 10 * 32768)
+    assert ut.ut_bsattn_bwd_varlen_workspace_size_stored(2, 0, 700, 3, 128, 10) == 0
+    assert ut.ut_bsattn_bwd_varlen_workspace_size_stored(0, 1000, 700, 3, 128, 10) == 0
 
 
 def _fwd(**kw):

@@ -19,15 +19,23 @@ pytestmark = pytest.mark.gpu
 DEV = "cuda"
 
 
-def run_gpu(case, backward=True):
+# dS tiles the backward's workspace makes room for: every pair (dQ from the
+# stored tiles), none (dQ recomputed) or half (the first query blocks stored,
+# the rest recomputed)
+MODES = {"stored": None, "recompute": 0, "partial": "half"}
+
+
+def run_gpu(case, backward=True, ds_pairs=None):
     q, k, v = (case[n].to(DEV) for n in ("q", "k", "v"))
     idx = ut.build_block_index(torch.from_numpy(case["block_mask"]).to(DEV))
     o, lse = ut.bsattn_fwd(q, k, v, idx, case["block"], case["scale"])
     out = {"o": o, "lse": lse, "idx": idx}
     if backward:
         do = case["do"].to(DEV)
+        if ds_pairs == "half":
+            ds_pairs = idx["nnz"] // 2
         out["dq"], out["dk"], out["dv"] = ut.bsattn_bwd(q, k, v, o, do, lse, idx, case["block"],
-                                                        case["scale"])
+                                                        case["scale"], ds_pairs=ds_pairs)
     torch.cuda.synchronize()
     return out
 
@@ -48,16 +56,17 @@ SMALL = [  # seed, N, H, D, block, density, batch, empty_rows
 ]
 
 
+@pytest.mark.parametrize("mode", list(MODES))
 @pytest.mark.parametrize("seed,n,H,D,block,density,batch,empty", SMALL)
-def test_small_fwd_bwd_elementwise(seed, n, H, D, block, density, batch, empty):
+def test_small_fwd_bwd_elementwise(seed, n, H, D, block, density, batch, empty, mode):
     case = W.random_case(seed, n, H, D, block, density, batch=batch, empty_rows=empty)
-    g = run_gpu(case)
+    g = run_gpu(case, ds_pairs=MODES[mode])
     O, L = oracle.bsattn_fwd(case["q"], case["k"], case["v"], case["block_mask"], block, case["scale"])
     check_out(g["o"], g["lse"], O, L, f"fwd {seed}")
     dQ, dK, dV = oracle.bsattn_bwd(case["q"], case["k"], case["v"], case["do"], case["block_mask"],
                                    block, case["scale"])
     for got, ref, nm in ((g["dq"], dQ, "dq"), (g["dk"], dK, "dk"), (g["dv"], dV, "dv")):
-        check_grad(got, ref, f"{nm} {seed}")
+        check_grad(got, ref, f"{nm} {seed} {mode}")
     if empty:
         # empty rows: O = 0, LSE = -inf, dQ = 0 exactly
         bm = case["block_mask"]

@@ -25,24 +25,28 @@ def _dev(case):
     return q, k, v, do, cu, idx
 
 
-def _run(case):
+def _run(case, ds_pairs=None):
     q, k, v, do, cu, idx = _dev(case)
     o, lse = ut.bsattn_fwd_varlen(q, k, v, cu, case["max_seqlen"], idx, case["block"], case["scale"])
+    if ds_pairs == "half":
+        ds_pairs = idx["nnz"] // 2
     dq, dk, dv = ut.bsattn_bwd_varlen(q, k, v, o, do, lse, cu, case["max_seqlen"], idx, case["block"],
-                                      case["scale"])
+                                      case["scale"], ds_pairs=ds_pairs)
     torch.cuda.synchronize()
     return o, lse, dq, dk, dv
 
 
+# dS tiles in the backward's workspace: all pairs, none (dQ recomputed), half
+@pytest.mark.parametrize("ds_pairs", [None, 0, "half"])
 @pytest.mark.parametrize("seed,lens,H,D,block,density", [
     (1, [700, 1300, 257, 0, 128], 2, 128, 128, 0.4),
     (2, [65, 1, 300, 64], 3, 64, 64, 0.5),
     (3, [1000, 999, 1001], 2, 128, 64, 0.3),
     (4, [129, 2000], 1, 64, 128, 0.25),
 ])
-def test_varlen_matches_oracle(seed, lens, H, D, block, density):
+def test_varlen_matches_oracle(seed, lens, H, D, block, density, ds_pairs):
     case = W.varlen_case(seed, lens, H, D, block, density)
-    o, lse, dq, dk, dv = _run(case)
+    o, lse, dq, dk, dv = _run(case, ds_pairs)
     args = (case["q"], case["k"], case["v"])
     O, L = oracle.bsattn_fwd_varlen(*args, case["cu_seqlens"], case["block_mask"], block,
                                     case["scale"])
