@@ -47,9 +47,6 @@ namespace ut {
 namespace {
 
 constexpr float kLog2e = 1.4426950408889634f;
-// s_waitcnt immediate (gfx9 encoding: vmcnt bits 3:0 and 15:14, expcnt 6:4,
-// lgkmcnt 11:8): vmcnt(4) lgkmcnt(0), expcnt not waited for.
-constexpr int kWaitVm4Lgkm0 = 0x0074;
 
 // ---------------------------------------------------------------------------
 // prep: two planes over the statistics rows, in the layout of LSE ([B, H, N]
@@ -372,13 +369,10 @@ __global__ __launch_bounds__(64 * (BLOCK / 32), 2) void bwd_dq_stored_kernel(
   using C = BwdCfg<D, BLOCK, NW>;
   constexpr int PAIRB = 2 * BLOCK * BLOCK;   // one pair's dS tile
   constexpr int WSB = 2 * 2048;              // one wave's dS chunks of one 64-key tile
-  // K tiles one tile ahead (two buffers), dS chunks two tiles ahead (three):
-  // the dS stream comes from HBM and needs more bytes in flight
   __shared__ __attribute__((aligned(1024))) char k_lds0[C::TILEB];
   __shared__ __attribute__((aligned(1024))) char k_lds1[C::TILEB];
   __shared__ __attribute__((aligned(1024))) char s_lds0[NW * WSB];
   __shared__ __attribute__((aligned(1024))) char s_lds1[NW * WSB];
-  __shared__ __attribute__((aligned(1024))) char s_lds2[NW * WSB];
 
   const int tid = threadIdx.x, lane = tid & 63;
   const int w = __builtin_amdgcn_readfirstlane(tid >> 6);
@@ -430,14 +424,13 @@ __global__ __launch_bounds__(64 * (BLOCK / 32), 2) void bwd_dq_stored_kernel(
 #pragma unroll
       for (int v = 0; v < C::IPW; ++v) buffer_load_lds16(rk, kdst + (w * C::IPW + v) * 1024, lo.dma[v]);
     };
-    // this wave's dS chunks of tile t: kSLoads direct loads, issued last
-    constexpr int kSLoads = WSB / 1024;
+    // this wave's two dS chunks of tile t, into its own part of the buffer
     auto load_s = [&](int t, char* sdst) __attribute__((always_inline)) {
       const int p = p0 + t / C::SUBS, hh = t % C::SUBS;
       const __amdgpu_buffer_rsrc_t rs =
           buffer_rsrc(ds + (int64_t)map[p] * PAIRB + (w * NW + 2 * hh) * 2048, WSB);
 #pragma unroll
-      for (int v = 0; v < kSLoads; ++v)
+      for (int v = 0; v < WSB / 1024; ++v)
         buffer_load_lds16(rs, sdst + w * WSB + v * 1024, v * 1024 + 16 * lane);
     };
 
@@ -465,57 +458,32 @@ __global__ __launch_bounds__(64 * (BLOCK / 32), 2) void bwd_dq_stored_kernel(
         }
       }
     };
-    auto sbuf = [&](auto slot) __attribute__((always_inline)) -> char* {
-      constexpr int S = decltype(slot)::value;
-      return S == 0 ? s_lds0 : S == 1 ? s_lds1 : s_lds2;
-    };
-    // Tile t uses K buffer t % 2 and dS buffer t % 3 (KP, SP).
-    auto iter = [&](int t, auto kpar, auto sslot) __attribute__((always_inline)) {
-      constexpr int KP = decltype(kpar)::value, SP = decltype(sslot)::value;
-      if (t + 1 < T) load_k(t + 1, KP ? k_lds0 : k_lds1);
-      const bool ahead = t + 2 < T;
-      if (ahead) load_s(t + 2, sbuf(std::integral_constant<int, (SP + 2) % 3>{}));
+    auto iter = [&](int t, auto par) __attribute__((always_inline)) {
+      constexpr int P = decltype(par)::value;
+      if (t + 1 < T) {
+        load_k(t + 1, P ? k_lds0 : k_lds1);
+        load_s(t + 1, P ? s_lds0 : s_lds1);
+      }
       // keep the loads ahead of this tile's work (the scheduler would sink them
       // to the wait at its end, exposing their latency)
       __builtin_amdgcn_sched_barrier(0);
-      step(KP ? k_lds1 : k_lds0, sbuf(sslot));
-      if (ahead) {
-        // Vector memory operations complete in issue order, so vmcnt(kSLoads)
-        // means every load but tile t + 2's dS has landed. The fences order
-        // LDS only: a full workgroup fence would wait for those loads too.
-        __builtin_amdgcn_s_waitcnt(kWaitVm4Lgkm0);
-        __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup", "local");
-        __builtin_amdgcn_s_barrier();
-        __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup", "local");
-      } else {
-        __builtin_amdgcn_s_waitcnt(0);
-        __syncthreads();
-      }
+      step(P ? k_lds1 : k_lds0, P ? s_lds1 : s_lds0);
+      __builtin_amdgcn_s_waitcnt(0);
+      __syncthreads();
     };
-    static_assert(kSLoads == 4, "the wait below counts four dS loads");
 
     load_k(0, k_lds0);
     load_s(0, s_lds0);
-    if (T > 1) load_s(1, s_lds1);
     __builtin_amdgcn_s_waitcnt(0);
     __syncthreads();
     using I0 = std::integral_constant<int, 0>;
     using I1 = std::integral_constant<int, 1>;
-    using I2 = std::integral_constant<int, 2>;
     int t = 0;
-    for (; t + 5 < T; t += 6) {
-      iter(t, I0{}, I0{});
-      iter(t + 1, I1{}, I1{});
-      iter(t + 2, I0{}, I2{});
-      iter(t + 3, I1{}, I0{});
-      iter(t + 4, I0{}, I1{});
-      iter(t + 5, I1{}, I2{});
+    for (; t + 1 < T; t += 2) {
+      iter(t, I0{});
+      iter(t + 1, I1{});
     }
-    if (t < T) iter(t, I0{}, I0{});
-    if (t + 1 < T) iter(t + 1, I1{}, I1{});
-    if (t + 2 < T) iter(t + 2, I0{}, I2{});
-    if (t + 3 < T) iter(t + 3, I1{}, I0{});
-    if (t + 4 < T) iter(t + 4, I0{}, I1{});
+    if (t < T) iter(t, I0{});
   }
 
 #pragma unroll
