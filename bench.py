@@ -49,16 +49,16 @@ PROFILED = {
     "workload": "c2k_train", "rho": "0.1",
     "sources": {
         "fwd": (('bsattn_fwd.hip', 'attn_util.h'), "f9edef214fda31434be0380d1ff002b0c4bcc9299f4ed051fd07afdc627af6c7"),
-        "bwd": (('bsattn_bwd.hip', 'attn_util.h'), "63fd222f48e98bb676d5fb34237407947012197dd8ad7d3e6d37f3e649cb5906"),
+        "bwd": (('bsattn_bwd.hip', 'attn_util.h'), "150731c2fbdbc5dce30a7f90f09b96484b3a25a9f28d08cd85e8f1bb22231f3b"),
         "btd": (('btd.hip',), "9d09820279dfbc138cc70ea771490b39ab8760643c11869db38ebddd4c222f50"),
     },
     "kernels": {
-        "bsattn_fwd<128,128>": {"read_bytes": 4.2974e+10, "write_bytes": 4.9016e+08, "clock_ghz": 1.66, "sources": "fwd"},
-        "bwd_dkdv_store<128,128>": {"read_bytes": 5.3878e+10, "write_bytes": 2.9874e+10, "clock_ghz": 1.63, "sources": "bwd"},
-        "bwd_dq_stored<128,128>": {"read_bytes": 5.1346e+10, "write_bytes": 4.7377e+08, "clock_ghz": 2.11, "sources": "bwd"},
-        "bwd_prep<128>": {"read_bytes": 1.006e+09, "write_bytes": 9.8641e+07, "clock_ghz": 2.10, "sources": "bwd"},
-        "gather_rows": {"read_bytes": 4.7588e+08, "write_bytes": 4.7349e+08, "clock_ghz": 2.43, "sources": "btd"},
-        "scatter_rows": {"read_bytes": 4.7586e+08, "write_bytes": 4.7348e+08, "clock_ghz": 2.35, "sources": "btd"},
+        "bsattn_fwd<128,128>": {"read_bytes": 4.2881e+10, "write_bytes": 4.9016e+08, "clock_ghz": 1.62, "sources": "fwd"},
+        "bwd_dkdv_store<128,128>": {"read_bytes": 5.384e+10, "write_bytes": 2.9874e+10, "clock_ghz": 1.59, "sources": "bwd"},
+        "bwd_dq_stored<128,128>": {"read_bytes": 5.1473e+10, "write_bytes": 4.7371e+08, "clock_ghz": 2.08, "sources": "bwd"},
+        "bwd_prep<128>": {"read_bytes": 1.006e+09, "write_bytes": 9.8641e+07, "clock_ghz": 1.99, "sources": "bwd"},
+        "gather_rows": {"read_bytes": 4.7588e+08, "write_bytes": 4.7349e+08, "clock_ghz": 2.31, "sources": "btd"},
+        "scatter_rows": {"read_bytes": 4.7586e+08, "write_bytes": 4.7348e+08, "clock_ghz": 2.19, "sources": "btd"},
     },
 }
 
