@@ -409,13 +409,28 @@ def kernel_rooflines(trace: list, steps: int, F: float, n: int, H: int, D: int,
         rate = work / (ms * 1e-3) / (1e12 if bound == "mfma" else 1e9)
         peak = PEAK_BF16_TFLOPS if bound == "mfma" else PEAK_HBM_GBS
         prof = profiled(nm, workload, rho)
+        traffic = (prof["read_bytes"] + prof["write_bytes"]) if prof else None
+        # the same kernel on the roofline of its measured traffic: intensity =
+        # algorithmic FLOP per byte beyond L2; below the ridge (peak FLOP/s over
+        # peak HBM bytes/s, ~315 FLOP/B) the attainable rate is intensity x HBM
+        # peak. Those bytes are L2 misses, much of them served by the MALL, and
+        # making every load an L2 hit barely speeds the attention kernels (see
+        # the design notes), so `bound` stays the matrix cores for them.
+        tr = None
+        if traffic and bound == "mfma":
+            inten = work / traffic
+            att = min(PEAK_BF16_TFLOPS, inten * PEAK_HBM_GBS / 1e3)
+            tr = {"flop_per_byte": round(inten, 1),
+                  "ridge_flop_per_byte": round(PEAK_BF16_TFLOPS * 1e3 / PEAK_HBM_GBS, 1),
+                  "attainable_tflops": round(att, 1), "frac_of_attainable": round(rate / att, 4),
+                  "gbs_beyond_l2": round(traffic / (ms * 1e-3) / 1e9, 1)}
         out.append({"kernel": nm, "bound": bound, "ms": round(ms, 4),
                     "launches_per_step": round(r["count"] / steps, 3),
                     "share_of_step_kernels": None, "work_per_launch": work,
                     "achieved": round(rate, 2), "peak": peak,
                     "unit": "TFLOP/s" if bound == "mfma" else "GB/s",
                     "frac": round(rate / peak, 4),
-                    "traffic": (prof["read_bytes"] + prof["write_bytes"]) if prof else None,
+                    "traffic": traffic, "traffic_roofline": tr,
                     "clock_ghz": prof.get("clock_ghz") if prof else None,
                     "total_ms": r["total_ms"]})
     return out
@@ -753,7 +768,8 @@ def main():
         # the step's dominant kernel (largest share of the traced kernel time)
         "roofline": {"bound": dom["bound"], "kernel": dom["kernel"], "achieved": dom["achieved"],
                      "peak": dom["peak"], "unit": dom["unit"], "frac": dom["frac"],
-                     "traffic": dom["traffic"], "ms": dom["ms"], "clock_ghz": dom["clock_ghz"],
+                     "traffic": dom["traffic"], "traffic_roofline": dom["traffic_roofline"],
+                     "ms": dom["ms"], "clock_ghz": dom["clock_ghz"],
                      "work_per_launch": dom["work_per_launch"]},
         "kernels": kernels,
         "trace_ms_per_step": {r["name"]: round(r["total_ms"] / args.steps, 4) for r in trace},
