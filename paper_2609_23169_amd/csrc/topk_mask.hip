@@ -35,27 +35,49 @@ constexpr int kSelMfmaThreads = 512;   // MFMA-path selection workgroup
 typedef __attribute__((__vector_size__(8 * sizeof(__bf16)))) __bf16 bf16x8_t;
 
 // pool(x)[b, h, i, d] = (1 / r_i) sum_{t in block i} x[b, t, h, d], written to
-// out[((b H + h) nblk + i) D + d] (pq for Q, pk for K).
+// out[((b H + h) nblk + i) D + d] (pq for Q, pk for K). Thread (g, c) of the
+// workgroup (blockDim.x = G * stride, stride >= chunks) sums 16-byte chunk c of
+// the rows of part g of the block (G parts of consecutive rows, so G times the
+// loads in flight); part 0 then adds the other parts' sums from LDS in the
+// order g = 1 .. G-1, so the result does not depend on timing.
 __global__ __launch_bounds__(kPoolMaxThreads) void pool_kernel(const __bf16* __restrict__ q,
                                                             const __bf16* __restrict__ k,
                                                             float* __restrict__ pq,
                                                             float* __restrict__ pk, int N, int H,
-                                                            int D, int block, int nblk) {
+                                                            int D, int block, int nblk, int stride) {
+  __shared__ float part[kPoolMaxThreads * 8];   // sums of parts 1 .. G-1: [g - 1][c][8]
   const int i = blockIdx.x, b = blockIdx.y;
   const __bf16* __restrict__ x = blockIdx.z ? k : q;
   float* __restrict__ out = blockIdx.z ? pk : pq;
   const int64_t row = (int64_t)H * D;              // elements per token
   const int t0 = i * block, r = min(N, t0 + block) - t0;
   const int chunks = H * D / 8, cpr = D / 8;       // 8-element chunks per token / per head
-  for (int c = threadIdx.x; c < chunks; c += blockDim.x) {
-    const __bf16* src = x + ((int64_t)b * N + t0) * row + 8 * c;
+  const int G = blockDim.x / stride;               // 1 whenever chunks > stride
+  const int g = threadIdx.x / stride;
+  const int ta = r * g / G, tb = r * (g + 1) / G;  // this part's rows
+  for (int c = threadIdx.x % stride; c - (int)(threadIdx.x % stride) < chunks; c += stride) {
     float acc[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
+    if (c < chunks) {
+      const __bf16* src = x + ((int64_t)b * N + t0) * row + 8 * c;
 #pragma unroll 16
-    for (int t = 0; t < r; ++t) {
-      const bf16x8_t v = *reinterpret_cast<const bf16x8_t*>(src + t * row);
+      for (int t = ta; t < tb; ++t) {
+        const bf16x8_t v = __builtin_nontemporal_load(reinterpret_cast<const bf16x8_t*>(src + t * row));
 #pragma unroll
-      for (int e = 0; e < 8; ++e) acc[e] += (float)v[e];
+        for (int e = 0; e < 8; ++e) acc[e] += (float)v[e];
+      }
     }
+    if (G > 1) {   // a single pass: stride >= chunks
+      if (g > 0 && c < chunks) {
+#pragma unroll
+        for (int e = 0; e < 8; ++e) part[((g - 1) * stride + c) * 8 + e] = acc[e];
+      }
+      __syncthreads();
+      if (g == 0 && c < chunks)
+        for (int gg = 1; gg < G; ++gg)
+#pragma unroll
+          for (int e = 0; e < 8; ++e) acc[e] += part[((gg - 1) * stride + c) * 8 + e];
+    }
+    if (g > 0 || c >= chunks) continue;
     const int h = c / cpr, d0 = 8 * (c % cpr);
     // true division keeps the mean correctly rounded (one rounding after the sum)
     float* dst = out + (((int64_t)b * H + h) * nblk + i) * D + d0;
@@ -288,14 +310,16 @@ hipError_t launch_topk_block_mask(const void* q, const void* k, int B, int N, in
   const int nblk = (N + block - 1) / block;
   float* pq = pooled;
   float* pk = pooled + (size_t)B * H * nblk * D;
-  // one 16-byte chunk of a token row per thread (up to 1024 threads)
+  // one 16-byte chunk of a token row per thread, the block's rows in up to
+  // four parts (at most 1024 threads); more chunks than that loop per thread
   const int chunks = H * D / 8;
-  const int pool_threads = (int)std::min<int64_t>(kPoolMaxThreads, (chunks + 63) / 64 * 64);
+  const int stride = (int)std::min<int64_t>(kPoolMaxThreads, (chunks + 63) / 64 * 64);
+  const int parts = std::max(1, std::min(4, kPoolMaxThreads / stride));
   {
     TraceScope ts_(s, "topk_pool");
-    hipLaunchKernelGGL(pool_kernel, dim3((unsigned)nblk, (unsigned)B, 2), dim3(pool_threads), 0, s,
+    hipLaunchKernelGGL(pool_kernel, dim3((unsigned)nblk, (unsigned)B, 2), dim3(stride * parts), 0, s,
                      static_cast<const __bf16*>(q), static_cast<const __bf16*>(k), pq, pk, N, H,
-                     D, block, nblk);
+                     D, block, nblk, stride);
   }
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
