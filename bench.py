@@ -784,7 +784,10 @@ def main():
     if not args.no_varlen:
         result["varlen"] = time_varlen(ut, W, dev, stream)
     if not args.no_cpu_baseline:
-        result["cpu_baseline"] = cpu_baseline(inst, args.cpu_seconds, attn_flops)
+        cb = cpu_baseline(inst, args.cpu_seconds, attn_flops)
+        # the same work's rate on the GPU (attention forward + backward) over the oracle's
+        cb["gpu_attention_over_oracle"] = round(result["attention"]["tflops_fwd_bwd"] / cb["value"], 1)
+        result["cpu_baseline"] = cb
     print(json.dumps(result), flush=True)
 
 
