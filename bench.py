@@ -53,12 +53,12 @@ PROFILED = {
         "btd": (('btd.hip',), "9d09820279dfbc138cc70ea771490b39ab8760643c11869db38ebddd4c222f50"),
     },
     "kernels": {
-        "bsattn_fwd<128,128>": {"read_bytes": 4.2881e+10, "write_bytes": 4.9016e+08, "clock_ghz": 1.62, "sources": "fwd"},
-        "bwd_dkdv_store<128,128>": {"read_bytes": 5.384e+10, "write_bytes": 2.9874e+10, "clock_ghz": 1.59, "sources": "bwd"},
-        "bwd_dq_stored<128,128>": {"read_bytes": 5.1473e+10, "write_bytes": 4.7371e+08, "clock_ghz": 2.08, "sources": "bwd"},
-        "bwd_prep<128>": {"read_bytes": 1.006e+09, "write_bytes": 9.8641e+07, "clock_ghz": 1.99, "sources": "bwd"},
-        "gather_rows": {"read_bytes": 4.7588e+08, "write_bytes": 4.7349e+08, "clock_ghz": 2.31, "sources": "btd"},
-        "scatter_rows": {"read_bytes": 4.7586e+08, "write_bytes": 4.7348e+08, "clock_ghz": 2.19, "sources": "btd"},
+        "bsattn_fwd<128,128>": {"read_bytes": 4.295e+10, "write_bytes": 4.9016e+08, "clock_ghz": 1.67, "sources": "fwd"},
+        "bwd_dkdv_store<128,128>": {"read_bytes": 5.3762e+10, "write_bytes": 2.9874e+10, "clock_ghz": 1.63, "sources": "bwd"},
+        "bwd_dq_stored<128,128>": {"read_bytes": 5.1505e+10, "write_bytes": 4.7375e+08, "clock_ghz": 2.13, "sources": "bwd"},
+        "bwd_prep<128>": {"read_bytes": 1.006e+09, "write_bytes": 9.8641e+07, "clock_ghz": 2.07, "sources": "bwd"},
+        "gather_rows": {"read_bytes": 4.7588e+08, "write_bytes": 4.735e+08, "clock_ghz": 2.41, "sources": "btd"},
+        "scatter_rows": {"read_bytes": 4.7586e+08, "write_bytes": 4.7348e+08, "clock_ghz": 2.39, "sources": "btd"},
     },
 }
 
