@@ -17,11 +17,14 @@ pytestmark = pytest.mark.gpu
 DEV = "cuda"
 
 
-def _run(case):
+def _run(case, ds_pairs=None):
     q, k, v, do = (case[n].to(DEV) for n in ("q", "k", "v", "do"))
     idx = ut.build_block_index(torch.from_numpy(case["block_mask"]).to(DEV))
     o, lse = ut.bsattn_fwd(q, k, v, idx, case["block"], case["scale"])
-    dq, dk, dv = ut.bsattn_bwd(q, k, v, o, do, lse, idx, case["block"], case["scale"])
+    if callable(ds_pairs):
+        ds_pairs = ds_pairs(idx["nnz"])
+    dq, dk, dv = ut.bsattn_bwd(q, k, v, o, do, lse, idx, case["block"], case["scale"],
+                               ds_pairs=ds_pairs)
     torch.cuda.synchronize()
     return q, k, v, do, idx, o, lse, dq, dk, dv
 
@@ -112,11 +115,23 @@ def test_non_default_stream_matches_default():
         assert torch.equal(a, b)
 
 
+def _dq_mode(mrng):
+    """One of the backward's dQ splits: every pair's dS tile stored (None),
+    none (0), or a random count (the rest recomputed)."""
+    m = int(mrng.integers(3))
+    if m == 2:
+        r = float(mrng.random())
+        return "some", lambda nnz: int(r * (nnz + 1))
+    return ("all", None) if m == 0 else ("none", 0)
+
+
 def test_random_shape_sweep():
     """Twenty seeded random configurations (length, heads, head_dim, block,
-    batch, density, forced-empty rows), forward and backward against the
-    oracle element by element."""
+    batch, density, forced-empty rows, dQ from all, none or some of the
+    stored dS tiles), forward and backward against the oracle element by
+    element."""
     rng = np.random.default_rng(2024)
+    mrng = np.random.default_rng(4048)   # modes drawn apart: the shapes stay as they were
     for case_no in range(20):
         n = int(rng.integers(1, 2500))
         H = int(rng.integers(1, 4))
@@ -127,10 +142,12 @@ def test_random_shape_sweep():
         nb = -(-n // blk)
         empty = int(rng.integers(0, min(3, nb) + 1))
         seed = int(rng.integers(1 << 30))
-        label = f"sweep {case_no}: n={n} H={H} D={D} block={blk} B={batch} density={dens:.2f} empty={empty}"
+        mode, pairs = _dq_mode(mrng)
+        label = (f"sweep {case_no}: n={n} H={H} D={D} block={blk} B={batch} density={dens:.2f} "
+                 f"empty={empty} dq={mode}")
         print(label, flush=True)
         case = W.random_case(seed, n, H, D, blk, dens, batch=batch, empty_rows=empty)
-        q, k, v, do, idx, o, lse, dq, dk, dv = _run(case)
+        q, k, v, do, idx, o, lse, dq, dk, dv = _run(case, pairs)
         O, L = oracle.bsattn_fwd(case["q"], case["k"], case["v"], case["block_mask"], blk, case["scale"])
         check_out(o, lse, O, L, label)
         grads = oracle.bsattn_bwd(case["q"], case["k"], case["v"], case["do"], case["block_mask"], blk,
@@ -141,8 +158,10 @@ def test_random_shape_sweep():
 
 def test_random_varlen_sweep():
     """Ten seeded random packed batches (1-5 samples of 0-1500 tokens, some
-    shorter than a block) against the oracle element by element."""
+    shorter than a block; dQ from all, none or some of the stored dS tiles)
+    against the oracle element by element."""
     rng = np.random.default_rng(2025)
+    mrng = np.random.default_rng(4050)
     for case_no in range(10):
         count = int(rng.integers(1, 6))
         lens = [int(x) for x in rng.integers(0, 1500, size=count)]
@@ -152,14 +171,16 @@ def test_random_varlen_sweep():
         D = int(rng.choice([64, 128]))
         blk = int(rng.choice([64, 128]))
         dens = float(rng.uniform(0.1, 0.9))
-        label = f"varlen sweep {case_no}: lens={lens} H={H} D={D} block={blk} density={dens:.2f}"
+        mode, pairs = _dq_mode(mrng)
+        label = f"varlen sweep {case_no}: lens={lens} H={H} D={D} block={blk} density={dens:.2f} dq={mode}"
         print(label, flush=True)
         c = W.varlen_case(int(rng.integers(1 << 30)), lens, H, D, blk, dens)
         q, k, v, do = (c[x].to(DEV) for x in ("q", "k", "v", "do"))
         cu = torch.from_numpy(c["cu_seqlens"]).to(DEV)
         idx = ut.build_block_index(torch.from_numpy(c["block_mask"]).to(DEV))
         o, lse = ut.bsattn_fwd_varlen(q, k, v, cu, c["max_seqlen"], idx, blk, c["scale"])
-        g = ut.bsattn_bwd_varlen(q, k, v, o, do, lse, cu, c["max_seqlen"], idx, blk, c["scale"])
+        g = ut.bsattn_bwd_varlen(q, k, v, o, do, lse, cu, c["max_seqlen"], idx, blk, c["scale"],
+                                 ds_pairs=pairs(idx["nnz"]) if callable(pairs) else pairs)
         torch.cuda.synchronize()
         O, L = oracle.bsattn_fwd_varlen(c["q"], c["k"], c["v"], c["cu_seqlens"], c["block_mask"], blk,
                                         c["scale"])
