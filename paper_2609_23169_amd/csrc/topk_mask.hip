@@ -95,12 +95,6 @@ __device__ inline uint32_t order_key(float f) {
   return (u & 0x80000000u) ? ~u : (u | 0x80000000u);
 }
 
-__device__ inline int wave_sum(int v) {
-#pragma unroll
-  for (int m = 32; m >= 1; m >>= 1) v += __shfl_xor(v, m, 64);
-  return v;
-}
-
 // Keys of one row: in registers (M64 > 0: at most 64 * M64 blocks) or read
 // from LDS each time (M64 == 0).
 template <int M64>
