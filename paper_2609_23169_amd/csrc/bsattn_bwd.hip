@@ -513,8 +513,10 @@ __global__ __launch_bounds__(64 * (BLOCK / 32), 2) void bwd_dq_stored_kernel(
 // four queries base(gq) + 16 x + (0..3) for key c16 and then for key
 // 16 + c16. Each store instruction writes 1 KB contiguously; the dQ pass
 // reads the chunk back with transposing LDS reads.
+// At every block size the kernel is built for two waves per SIMD (the launch
+// bound's second argument): up to 256 VGPRs per wave.
 template <int D, int BLOCK, bool STORE>
-__global__ __launch_bounds__(64 * (BLOCK / 32), 256 / BLOCK) void bwd_dkdv_kernel(
+__global__ __launch_bounds__(64 * (BLOCK / 32), 2) void bwd_dkdv_kernel(
     const __bf16* __restrict__ Q, const __bf16* __restrict__ K, const __bf16* __restrict__ V,
     const __bf16* __restrict__ dO, const float* __restrict__ aux, __bf16* __restrict__ dK,
     __bf16* __restrict__ dV, int B, int N_all, int H, int nblk, float scale,
