@@ -49,16 +49,16 @@ PROFILED = {
     "workload": "c2k_train", "rho": "0.1",
     "sources": {
         "fwd": (('bsattn_fwd.hip', 'attn_util.h'), "f9edef214fda31434be0380d1ff002b0c4bcc9299f4ed051fd07afdc627af6c7"),
-        "bwd": (('bsattn_bwd.hip', 'attn_util.h'), "150731c2fbdbc5dce30a7f90f09b96484b3a25a9f28d08cd85e8f1bb22231f3b"),
+        "bwd": (('bsattn_bwd.hip', 'attn_util.h'), "30449738a785bc8ec6d86a7b61c70e144339b1436c276f6c070267757550ba09"),
         "btd": (('btd.hip',), "9d09820279dfbc138cc70ea771490b39ab8760643c11869db38ebddd4c222f50"),
     },
     "kernels": {
-        "bsattn_fwd<128,128>": {"read_bytes": 4.295e+10, "write_bytes": 4.9016e+08, "clock_ghz": 1.67, "sources": "fwd"},
-        "bwd_dkdv_store<128,128>": {"read_bytes": 5.3762e+10, "write_bytes": 2.9874e+10, "clock_ghz": 1.63, "sources": "bwd"},
-        "bwd_dq_stored<128,128>": {"read_bytes": 5.1505e+10, "write_bytes": 4.7375e+08, "clock_ghz": 2.13, "sources": "bwd"},
+        "bsattn_fwd<128,128>": {"read_bytes": 4.2933e+10, "write_bytes": 4.9016e+08, "clock_ghz": 1.69, "sources": "fwd"},
+        "bwd_dkdv_store<128,128>": {"read_bytes": 5.3768e+10, "write_bytes": 2.9874e+10, "clock_ghz": 1.63, "sources": "bwd"},
+        "bwd_dq_stored<128,128>": {"read_bytes": 5.1511e+10, "write_bytes": 4.7375e+08, "clock_ghz": 2.13, "sources": "bwd"},
         "bwd_prep<128>": {"read_bytes": 1.006e+09, "write_bytes": 9.8641e+07, "clock_ghz": 2.07, "sources": "bwd"},
-        "gather_rows": {"read_bytes": 4.7588e+08, "write_bytes": 4.735e+08, "clock_ghz": 2.41, "sources": "btd"},
-        "scatter_rows": {"read_bytes": 4.7586e+08, "write_bytes": 4.7348e+08, "clock_ghz": 2.39, "sources": "btd"},
+        "gather_rows": {"read_bytes": 4.7588e+08, "write_bytes": 4.7349e+08, "clock_ghz": 2.45, "sources": "btd"},
+        "scatter_rows": {"read_bytes": 4.7586e+08, "write_bytes": 4.7348e+08, "clock_ghz": 2.30, "sources": "btd"},
     },
 }
 
