@@ -25,7 +25,15 @@ def _check(bm):
 @pytest.mark.parametrize("B,H,Nq,Nk,p", [(1, 1, 1, 1, 1.0), (1, 1, 1, 1, 0.0), (1, 3, 7, 7, 0.3),
                                          (2, 2, 13, 70, 0.5), (1, 4, 65, 63, 0.2),
                                          (1, 2, 130, 130, 1.0), (1, 1, 200, 200, 0.0),
-                                         (3, 5, 64, 64, 0.5), (1, 2, 129, 1, 0.7)])
+                                         (3, 5, 64, 64, 0.5), (1, 2, 129, 1, 0.7),
+                                         # more than 16 row tiles: waves of the column
+                                         # lists walk two or three tiles each
+                                         (1, 2, 1100, 90, 0.3), (1, 1, 3000, 40, 0.1),
+                                         (1, 1, 2048, 64, 1.0),
+                                         # 17,600 row counts: the scan takes two passes
+                                         (2, 8, 1100, 33, 0.05),
+                                         # 1,500 columns: three passes of row chunks
+                                         (1, 1, 50, 1500, 0.4)])
 def test_random_masks(B, H, Nq, Nk, p):
     rng = np.random.default_rng(B * 100 + H * 10 + Nq)
     _check((rng.random((B, H, Nq, Nk)) < p).astype(np.uint8) * 3)
