@@ -48,8 +48,8 @@ CAL_COPY_BYTES = 1 << 28      # calibration copy: 256 MiB read + 256 MiB written
 PROFILED = {
     "workload": "c2k_train", "rho": "0.1",
     "sources": {
-        "fwd": (('bsattn_fwd.hip', 'attn_util.h'), "f9edef214fda31434be0380d1ff002b0c4bcc9299f4ed051fd07afdc627af6c7"),
-        "bwd": (('bsattn_bwd.hip', 'attn_util.h'), "30449738a785bc8ec6d86a7b61c70e144339b1436c276f6c070267757550ba09"),
+        "fwd": (('bsattn_fwd.hip', 'attn_util.h'), "5c79cb75d52dbd6532c51f8b608d957a550094d53c4729ea94a07d6061e285de"),
+        "bwd": (('bsattn_bwd.hip', 'attn_util.h'), "f53406920837e147b459754918010fd9958ddb0da03c46d2c24502c8992cb1cb"),
         "btd": (('btd.hip',), "9d09820279dfbc138cc70ea771490b39ab8760643c11869db38ebddd4c222f50"),
     },
     "kernels": {

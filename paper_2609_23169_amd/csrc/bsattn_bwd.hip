@@ -1,6 +1,7 @@
 // Block-sparse attention backward on gfx950: gradients of Eq. 8 (paper
-// Sec. 3.3) with the block mask held constant. Three launches, no atomics,
-// deterministic:
+// Sec. 3.3) with the block mask held constant. No atomics, deterministic.
+// Three launches with the minimum workspace (five when it holds dS tiles,
+// below):
 //
 //   prep  : per query row, LSE log2(e) and -delta = -sum_d dO[r,d] O[r,d]
 //           (fp32, two planes of the workspace);

@@ -14,13 +14,14 @@
 // layout (lane = one query, 16 keys) to the B-operand layout of two 16-query
 // groups (lane = one query of each group, 8 keys), with the keys in an
 // order whose V^T operand the transposing ds_read_b64_tr_b16 reads without
-// bank conflicts. (The score product stays on 32x32x16: its K operand read
-// in the 16x16x32 layout, four lane groups on the same 16 rows, costs LDS
-// bank-conflict cycles.)
+// bank conflicts. (The score product stays on 32x32x16: a forward with both
+// products on 16x16x32, K in a conflict-free layout, held a higher clock but
+// kept the matrix cores busy a smaller share of the time, and was slower.)
 //
 // The loop is built to spend as few vector instructions per MFMA as
-// possible, since the vector ALU (softmax) and not the matrix core is the
-// scarce resource at head_dim 128:
+// possible: at head_dim 128 the softmax's vector work per score once set the
+// kernel's pace, and under the board's power limit every instruction costs
+// clock:
 //  * K and V tiles (64 keys) go from global memory straight into LDS with
 //    buffer loads; the tile base lives in the scalar buffer descriptor, so
 //    the per-lane offsets are loop invariant, and rows past N fall outside
