@@ -232,7 +232,9 @@ def time_fg_step(ut, fg_mask, grid: int, dev, stream, C: int = 64, reps: int = 2
         e1.record(stream)
         torch.cuda.synchronize()
         ms = e0.elapsed_time(e1) / reps
-        out[name] = {"ms": round(ms, 4), "bytes": nbytes, "gbs": round(nbytes / (ms * 1e-3) / 1e9, 1)}
+        gbs = nbytes / (ms * 1e-3) / 1e9
+        out[name] = {"ms": round(ms, 4), "bytes": nbytes, "gbs": round(gbs, 1),
+                     "frac_hbm": round(gbs / PEAK_HBM_GBS, 4)}
     return out
 
 
@@ -278,7 +280,9 @@ def time_decode_prep(ut, fg_mask, grid: int, dev, stream, C: int = 64) -> dict:
         if st != ut.UT_OK:
             raise ut.UltraTexError(name, st, ut.last_error())
         ms = _time(run, stream)
-        out[name] = {"ms": round(ms, 4), "bytes": int(nbytes), "gbs": round(nbytes / (ms * 1e-3) / 1e9, 1)}
+        gbs = nbytes / (ms * 1e-3) / 1e9
+        out[name] = {"ms": round(ms, 4), "bytes": int(nbytes), "gbs": round(gbs, 1),
+                     "frac_hbm": round(gbs / PEAK_HBM_GBS, 4)}
     return out
 
 
